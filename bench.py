@@ -1,0 +1,298 @@
+#!/usr/bin/env python3
+"""Benchmark of the EDiT outer synchronization step on one MI355X.
+
+One step = one outer round over every sync unit of the workload (default:
+Llama-1B-shaped, 24 units x 51,384,320 parameters, K = 8 bf16 replicas, fp32
+theta and momentum), issued in forward order over HIP streams.  Between
+steps (untimed) the seeded generator rewrites every replica as
+cast(theta_t + s_j * N(0, 1e-3)), i.e. what K workers would hold after their
+inner steps; the timed region is the outer step alone, with all inputs
+resident in HBM.
+
+Prints ONE JSON line (see the field notes in the design doc).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
+METRIC = "outer-sync ms/step and achieved HBM GB/s (% of peak), 1B model K=8"
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2412_07210_amd", "csrc", "edit_outer_kernels.hip")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_counters.json")
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def unit_bytes(n: int, K: int, R: int, active: int, rolled_back: bool) -> tuple:
+    """Algorithmic HBM bytes of one unit's step: (pass 1, pass 2).
+
+    pass 1 reads theta (4 B) and the K replicas; pass 2 reads theta, b and the
+    replicas of contributing workers, writes theta, b and all K replicas.  On
+    a rollback pass 2 reads theta and writes the K replicas only.
+    """
+    p1 = n * (4 + K * R)
+    if rolled_back:
+        p2 = n * (4 + K * R)
+    else:
+        p2 = n * (8 + active * R + 8 + K * R)
+    return p1, p2
+
+
+def measured_traffic(per_launch_units: float):
+    """HBM bytes per pass-2 launch from committed rocprofv3 counters, if they
+    were taken on the current kernel source; else None."""
+    try:
+        with open(COUNTERS_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if data.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return float(data["pass2_bytes_per_launch"])
+    except (KeyError, TypeError, ValueError):
+        return None
+
+
+def copy_probe_gbps(torch, outer, nbytes: int = 2 << 30, reps: int = 5) -> float:
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    outer.copy_probe(dst, src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        outer.copy_probe(dst, src)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del src, dst
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def cpu_baseline(samples, wl, seconds_hint: float):
+    """Time the CPU oracle (one thread, as it stands) on the captured units."""
+    import numpy as np
+    from oracle import OracleConfig, OracleUnit
+
+    K, R = wl.num_workers, wl.replica_bytes
+    total_bytes, total_s, done = 0, 0.0, 0
+    for (u, theta, mom, reps) in samples:
+        unit = OracleUnit(K, OracleConfig(**wl.hyper()))
+        t0 = time.perf_counter()
+        unit.step(theta, mom, reps)
+        dt = time.perf_counter() - t0
+        total_s += dt
+        total_bytes += theta.size * (3 * K * R + 20)
+        done += 1
+        log(f"cpu oracle unit {u}: {dt:.2f} s")
+        if total_s > seconds_hint:
+            break
+    per_unit_s = total_s / done
+    return {
+        "value": round(total_bytes / total_s / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "ms_per_step_extrapolated": round(per_unit_s * wl.num_units * 1e3, 1),
+        "sample": f"{done} of {wl.num_units} units of one round ({samples[0][1].size:,} elements each, "
+                  f"K={K}), single-threaded C oracle, fp64",
+    }
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[1])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=90)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="c3", help="workload: c1..c5")
+    ap.add_argument("--streams", type=int, default=2, help="HIP streams for the unit pipeline")
+    ap.add_argument("--units", type=int, default=0, help="use only the first N units (0 = all)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-kernel-events", action="store_true",
+                    help="do not record per-kernel HIP events (roofline then null)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU-baseline time budget")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-copy-probe", action="store_true")
+    args = ap.parse_args(argv)
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU: the outer step reduces "
+                                   "all K replicas in one GPU's HBM; --gpus must be 1"}), flush=True)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2412_07210_amd import EditOuter, OuterConfig, outer, synth
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}), flush=True)
+        return 3
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    wl = synth.get(args.config)
+    if args.units:
+        wl = wl.with_units(range(args.units))
+    K, R = wl.num_workers, wl.replica_bytes
+    hyper = wl.hyper()
+    warm_rounds = hyper.pop("warmup_rounds")
+    lib = EditOuter(OuterConfig(num_workers=K, layer_numel=wl.layer_numel, replica_dtype=wl.replica_dtype,
+                                ema_warmup_rounds=warm_rounds, **hyper), dev)
+    log(f"workload {wl.name}: {wl.num_units} units, {wl.total_numel:,} params, K={K}, {wl.replica_dtype}")
+
+    units = []
+    for u in range(wl.num_units):
+        th = wl.init_theta(u, dev, args.seed)
+        reps = [torch.empty(th.numel(), dtype=wl.torch_dtype, device=dev) for _ in range(K)]
+        units.append((th, torch.zeros_like(th), reps))
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(device=dev) for _ in range(args.streams)] if args.streams > 1 else None
+    events = not args.no_kernel_events
+    lib.set_profiling(events)
+
+    step_ms, p1_ms, p2_ms, dec_ms = [], [], [], []
+    p1_bytes = p2_bytes = step_bytes = nominal_bytes = 0
+    p1_launches = p2_launches = 0
+    masked_total = rollbacks = 0
+    samples = []
+    total_rounds = args.warmup + args.steps
+    t_start = time.time()
+    for t in range(total_rounds):
+        std = wl.worker_std(t, args.seed)
+        for u, (th, b, reps) in enumerate(units):
+            wl.fill_replicas(th, reps, u, t, args.seed, std=std)
+        timed = t >= args.warmup
+        if timed and t == args.warmup and not args.no_cpu_baseline:
+            for u in range(min(3, wl.num_units)):
+                th, b, reps = units[u]
+                hb = [r.view(torch.int16).cpu().numpy().view(np.uint16) if r.dtype == torch.bfloat16
+                      else r.cpu().numpy() for r in reps]
+                samples.append((u, th.cpu().numpy().copy(), b.cpu().numpy().copy(), hb))
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        z = torch.cuda.Event(enable_timing=True)
+        a.record()
+        lib.step_round(units, streams=streams)
+        z.record()
+        torch.cuda.synchronize()
+        if not timed:
+            continue
+        step_ms.append(a.elapsed_time(z))
+        for u, (th, b, reps) in enumerate(units):
+            st = lib.state_get(u)
+            active = int(np.count_nonzero(st.weight > 0)) if st.clip_coef > 0 else 0
+            b1, b2 = unit_bytes(th.numel(), K, R, active, st.rolled_back)
+            p1_bytes += b1
+            p2_bytes += b2
+            step_bytes += b1 + b2
+            nominal_bytes += th.numel() * (3 * K * R + 20)
+            masked_total += int(st.anomalous.sum())
+            rollbacks += int(st.rolled_back)
+            if events:
+                k1, kd, k2 = lib.kernel_times(u)
+                p1_ms.append(k1)
+                dec_ms.append(kd)
+                p2_ms.append(k2)
+            p1_launches += 1
+            p2_launches += 1
+        if (t - args.warmup) % 10 == 0:
+            log(f"round {t}: {step_ms[-1]:.3f} ms")
+    wall = time.time() - t_start
+
+    total_ms = sum(step_ms)
+    ms_per_step = total_ms / len(step_ms)
+    value = step_bytes / (total_ms * 1e-3) / 1e9
+    min_bytes = sum(th.numel() * (2 * K * R + 16) for th, _, _ in units) * len(step_ms)
+    q = np.percentile(step_ms, [10, 50, 90])
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: {wl.description}",
+            "units": wl.num_units,
+            "unit_numel": wl.layer_numel[0],
+            "total_params": wl.total_numel,
+            "num_workers": K,
+            "replica_dtype": wl.replica_dtype,
+            "master_dtype": "f32",
+            "streams": args.streams,
+            "parallelism": "single GPU, K replicas reduced in HBM",
+        },
+        "ms_p10": round(float(q[0]), 4),
+        "ms_p50": round(float(q[1]), 4),
+        "ms_p90": round(float(q[2]), 4),
+        "pct_peak_hbm": round(100 * value / PEAK_HBM_GBPS, 2),
+        "gbps_on_min_bytes": round(min_bytes / (total_ms * 1e-3) / 1e9, 2),
+        "gbps_on_nominal_design_bytes": round(nominal_bytes / (total_ms * 1e-3) / 1e9, 2),
+        "masked_workers_total": masked_total,
+        "rollbacks_total": rollbacks,
+        "wall_s": round(wall, 1),
+    }
+    if events and p2_ms:
+        per_launch = p2_bytes / p2_launches
+        avg_ms = sum(p2_ms) / len(p2_ms)
+        achieved = per_launch / (avg_ms * 1e-3) / 1e9
+        traffic = measured_traffic(per_launch)
+        result["roofline"] = {
+            "kernel": "pass2_update_kernel (fused average + clip + Nesterov + write-back)",
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4),
+            "traffic": traffic,
+            "bytes_per_launch": int(per_launch),
+            "avg_launch_ms": round(avg_ms, 5),
+        }
+        result["kernels_ms_avg"] = {
+            "pass1_gram": round(sum(p1_ms) / len(p1_ms), 5),
+            "decide": round(sum(dec_ms) / len(dec_ms), 5),
+            "pass2_update": round(avg_ms, 5),
+            "pass1_gbps": round((p1_bytes / p1_launches) / (sum(p1_ms) / len(p1_ms) * 1e-3) / 1e9, 2),
+        }
+    else:
+        result["roofline"] = None
+    if not args.no_copy_probe:
+        result["copy_probe_gbps"] = round(copy_probe_gbps(torch, outer), 1)
+    lib.close()
+    del units
+    torch.cuda.empty_cache()
+    if samples:
+        result["cpu_baseline"] = cpu_baseline(samples, wl, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,152 @@
+/*
+ * edit_outer.h -- C ABI of the EDiT layer-wise outer synchronization step
+ * on one AMD Instinct MI355X (gfx950).
+ *
+ * The operation (EDiT, arXiv 2412.07210, Sec. 3.2 "Pseudo Gradient Penalty",
+ * Eq. 1-5, and the Sync() procedure of the appendix, Algorithm 2):
+ * K workers each hold a replica r_j of one module's parameters after their
+ * local steps; theta is the module's last synchronized value.  One call
+ *   1. forms the pseudo gradients Delta_j = r_j - theta and their norms
+ *      G_j = ||Delta_j||_2 over the whole module,
+ *   2. flags anomalous workers by an EMA z-test on G_j (Eq. 1; no flags
+ *      during a warm-up of `ema_warmup_rounds` rounds) and updates the EMA
+ *      mean/std of the unflagged workers,
+ *   3. rolls every replica back to theta when all workers are flagged,
+ *   4. otherwise weights the unflagged workers by a softmax of -G_j (Eq. 2),
+ *      averages Delta_bar = sum_j w_j Delta_j (Eq. 3), clips it by
+ *      beta = min(phi / (||Delta_bar|| + eps), 1) (Eq. 4-5),
+ *   5. applies the outer optimizer, SGD with Nesterov momentum on the outer
+ *      gradient g = -beta*Delta_bar (Sec. 4.1):
+ *        b' = rho*b + g;   theta' = theta - nu*(g + rho*b'),
+ *   6. writes theta' back to every replica (all K, flagged ones included).
+ *
+ * Precision: theta and the momentum b are fp32; replicas are fp32 or bf16
+ * (round-to-nearest-even of the fp32 theta').  Norms, EMA state, weights and
+ * the clip factor are fp64; the elementwise update is fp32.
+ *
+ * All pointers to tensor data are DEVICE pointers on the device that was
+ * current when the handle was created; the caller owns them.  The library
+ * owns the handle, the EMA state, its scratch memory and its events.
+ * Every function returns an edit_status_t; nothing is thrown across the ABI.
+ * On failure, edit_outer_last_error() returns a message for the calling
+ * thread.
+ */
+#ifndef EDIT_OUTER_H
+#define EDIT_OUTER_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Largest number of workers per sync group the kernels are built for. */
+#define EDIT_MAX_K 16
+
+/* Penalty components; clearing all three gives the DiLoCo outer step
+ * (the ablations of Sec. 4.5). */
+#define EDIT_AE 1u /* anomaly elimination (EMA z-test, rollback)  */
+#define EDIT_WA 2u /* norm-based weighted averaging (Eq. 2)        */
+#define EDIT_GC 4u /* pseudo-gradient clip (Eq. 4-5)               */
+
+typedef struct edit_outer *edit_outer_t; /* opaque, library-owned */
+
+typedef enum {
+  EDIT_OK = 0,
+  EDIT_EINVAL = -1, /* bad argument: index, size, NULL, alignment, aliasing  */
+  EDIT_ENOMEM = -2, /* host or device allocation failed                      */
+  EDIT_EHIP = -3,   /* a HIP runtime call or a kernel launch failed           */
+  EDIT_ESTATE = -4, /* not valid now (e.g. state_get before any step)         */
+  EDIT_ENODEV = -5  /* the current device is not a gfx950 GPU                 */
+} edit_status_t;
+
+typedef enum { EDIT_F32 = 0, EDIT_BF16 = 1 } edit_dtype_t;
+
+typedef struct {
+  int32_t num_workers;        /* K, 1..EDIT_MAX_K                              */
+  int32_t num_layers;         /* L sync units (modules), >= 1                  */
+  const int64_t *layer_numel; /* [L] elements per unit (>= 0); copied at init  */
+  int32_t replica_dtype;      /* edit_dtype_t of the K replicas                */
+  uint32_t flags;             /* EDIT_AE | EDIT_WA | EDIT_GC                   */
+  double outer_lr;            /* nu  (paper: 0.8 or 1.0)                       */
+  double momentum;            /* rho (paper: 0.85 or 0.8)                      */
+  double clip_threshold;      /* phi of Eq. 4 (paper: 10)                      */
+  double clip_eps;            /* eps of Eq. 4, > 0                             */
+  double ema_alpha;           /* alpha of Eq. 1 (paper: 0.02), in (0, 1]       */
+  double z_threshold;         /* delta of the z-test (paper: 3)                */
+  int64_t ema_warmup_rounds;  /* rounds per unit with no anomaly flagging      */
+} edit_outer_config_t;
+
+/* Per-unit state and the decision of its most recent step (host memory). */
+typedef struct {
+  int64_t round;               /* completed outer rounds of this unit         */
+  int32_t num_workers;         /* K                                           */
+  int32_t rolled_back;         /* 1 if every worker was flagged               */
+  int32_t z_tested;            /* 1 if the z-test was applied (after warm-up) */
+  int32_t reserved;
+  double ema_mean[EDIT_MAX_K]; /* mu_j after the last step                    */
+  double ema_std[EDIT_MAX_K];  /* sigma_j after the last step                 */
+  double norm[EDIT_MAX_K];     /* G_j of the last step                        */
+  double weight[EDIT_MAX_K];   /* w_j of the last step (0 when flagged)       */
+  uint8_t anomalous[EDIT_MAX_K];
+  double synced_norm;          /* ||Delta_bar|| of the last step              */
+  double clip_coef;            /* beta of the last step (0 on rollback)       */
+} edit_layer_state_t;
+
+/* Create a handle on the current device.  Validates cfg (K range, L >= 1,
+ * numel >= 0, dtype, 0 < alpha <= 1, eps > 0, non-negative warm-up),
+ * allocates the EMA state (zero), per-unit scratch and events.
+ * EDIT_EINVAL for a bad config, EDIT_ENODEV off gfx950, EDIT_ENOMEM. */
+edit_status_t edit_outer_init(const edit_outer_config_t *cfg, edit_outer_t *out);
+
+/* One outer step of unit `layer` (Sec. 3.2, Algorithm 2), enqueued on
+ * `stream` (a hipStream_t; NULL = the default stream).  No host
+ * synchronisation; the three kernels (norm/Gram pass, decision, update pass)
+ * run in stream order.
+ *   theta    [n] fp32, in: theta_t, out: theta_{t+1} (unchanged on rollback)
+ *   momentum [n] fp32, in/out: outer momentum b (zero-initialised by caller)
+ *   replicas host array of K device pointers, each [n] of replica_dtype;
+ *            in: the workers' parameters, out: theta_{t+1} in that dtype
+ * Device pointers must be 16-byte aligned and the K+2 ranges disjoint
+ * (else EDIT_EINVAL).  Steps of one unit must be ordered by the caller
+ * (same stream or events); different units may run concurrently on
+ * different streams.  n = 0 is allowed (NULL pointers accepted). */
+edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float *theta,
+                                    float *momentum, void *const *replicas, void *stream);
+
+/* Copy unit `layer`'s EMA state and last decision to *out, after waiting for
+ * that unit's last enqueued step.  EDIT_ESTATE if the unit never stepped and
+ * no state was set. */
+edit_status_t edit_outer_state_get(edit_outer_t h, int32_t layer, edit_layer_state_t *out);
+
+/* Restore unit `layer`'s EMA state (ema_mean, ema_std, round; other fields
+ * ignored), e.g. when resuming from a checkpoint.  Waits for that unit's
+ * last enqueued step first. */
+edit_status_t edit_outer_state_set(edit_outer_t h, int32_t layer, const edit_layer_state_t *in);
+
+/* Release everything the handle owns (waits for its pending work). */
+void edit_outer_destroy(edit_outer_t h);
+
+const char *edit_outer_strerror(edit_status_t s);
+
+/* Message of the last failure on the calling thread ("" if none). */
+const char *edit_outer_last_error(void);
+
+/* ---- measurement helpers (not part of the method) ---------------------- */
+
+/* When enabled, each step records HIP events around its three kernels. */
+edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t enable);
+
+/* Durations in ms of the last profiled step of `layer`: ms[0] the norm/Gram
+ * pass, ms[1] the decision kernel, ms[2] the update pass.  Waits for it. */
+edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[3]);
+
+/* Plain device-to-device copy kernel of nbytes (a multiple of 16, 16-byte
+ * aligned pointers), used to calibrate HBM traffic counters and bandwidth. */
+edit_status_t edit_outer_copy_probe(void *dst, const void *src, int64_t nbytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EDIT_OUTER_H */

@@ -116,11 +116,14 @@ static void ema_update(double G, double alpha, double *mu, double *sigma) {
 
 /* ------------------------------------------------------------ the step */
 
-static void write_back(void *replica, int is_bf16, int64_t i, float value) {
-  if (is_bf16)
-    ((uint16_t *)replica)[i] = oracle_f32_to_bf16(value);
-  else
-    ((float *)replica)[i] = value;
+/* Every worker takes the same value: theta_{t+1}[i] in the replica type. */
+static void write_back_all(void *const *replicas, int K, int is_bf16, int64_t i, float value) {
+  if (is_bf16) {
+    uint16_t h = oracle_f32_to_bf16(value);
+    for (int j = 0; j < K; ++j) ((uint16_t *)replicas[j])[i] = h;
+  } else {
+    for (int j = 0; j < K; ++j) ((float *)replicas[j])[i] = value;
+  }
 }
 
 int oracle_step(const oracle_cfg_t *cfg, int K, int64_t n, int replica_is_bf16,
@@ -168,8 +171,7 @@ int oracle_step(const oracle_cfg_t *cfg, int K, int64_t n, int replica_is_bf16,
 
   if (n_ok == 0) {
     /* Rollback: every worker returns to the last synchronized theta_t. */
-    for (int64_t i = 0; i < n; ++i)
-      for (int j = 0; j < K; ++j) write_back(replicas[j], bf16, i, theta[i]);
+    for (int64_t i = 0; i < n; ++i) write_back_all(replicas, K, bf16, i, theta[i]);
     r.rolled_back = 1;
     ema->round += 1;
     if (rec) *rec = r;
@@ -224,7 +226,7 @@ int oracle_step(const oracle_cfg_t *cfg, int K, int64_t n, int replica_is_bf16,
     double th_new = (double)theta[i] - nu * (g + rho * b_new);
     theta[i] = (float)th_new;
     momentum[i] = (float)b_new;
-    for (int j = 0; j < K; ++j) write_back(replicas[j], bf16, i, theta[i]);
+    write_back_all(replicas, K, bf16, i, theta[i]);
   }
   free(dbar);
 

@@ -1,0 +1,60 @@
+// Internal declarations shared by the kernels and the host runtime of
+// libedit_outer.so.  Not part of the public ABI (include/edit_outer.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "edit_outer.h"
+
+namespace edit {
+
+constexpr int kThreads = 256;        // threads per block of the streaming passes
+constexpr int kMaxK = EDIT_MAX_K;
+constexpr int kMaxPairs = kMaxK * (kMaxK + 1) / 2;
+
+// Device-resident state and decision of one sync unit.  Written by the
+// decision kernel, read by the update pass and copied out by state_get.
+struct alignas(16) UnitRecord {
+  double mu[kMaxK];         // EMA mean of G_j (Eq. 1)
+  double sigma[kMaxK];      // EMA std of G_j (Eq. 1)
+  double norm[kMaxK];       // G_j of the last step
+  double weight[kMaxK];     // w_j of the last step
+  double synced_norm;       // ||Delta_bar||
+  double clip_coef;         // beta
+  int64_t round;            // completed rounds of this unit
+  float coef[kMaxK];        // beta * w_j in fp32, consumed by the update pass
+  int32_t src[kMaxK];       // worker whose data the update pass loads for slot j
+  int32_t rollback;         // 1: every worker flagged, reset replicas only
+  int32_t use_deltas;       // 0: no worker has a non-zero coefficient
+  int32_t z_tested;
+  int32_t stepped;          // at least one step or state_set happened
+  uint8_t anomalous[kMaxK];
+};
+
+struct DecideParams {
+  double alpha, delta, phi, eps;
+  int64_t warmup;
+  uint32_t flags;
+};
+
+// Launchers (kernels.hip).  All enqueue on `stream` and return the launch
+// status; none synchronises.
+hipError_t launch_pass1(int K, bool bf16, int blocks, const float* theta,
+                        const void* const* reps, int64_t n, double* partials,
+                        hipStream_t stream);
+hipError_t launch_decide(int K, const double* partials, int rows, UnitRecord* rec,
+                         const DecideParams& prm, hipStream_t stream);
+hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom,
+                        void* const* reps, const UnitRecord* rec, int64_t n, float lr,
+                        float rho, hipStream_t stream);
+hipError_t launch_copy(void* dst, const void* src, int64_t nbytes, int blocks,
+                       hipStream_t stream);
+
+// Resident blocks per CU of each streaming kernel (for the persistent grids).
+int pass1_blocks_per_cu(int K, bool bf16);
+int pass2_blocks_per_cu(int K, bool bf16);
+
+inline int num_pairs(int K) { return K * (K + 1) / 2; }
+
+}  // namespace edit

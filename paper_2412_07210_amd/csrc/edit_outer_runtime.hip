@@ -1,0 +1,371 @@
+// Host runtime of libedit_outer.so: the C ABI declared in include/edit_outer.h.
+//
+// A handle owns, per sync unit: the device record (EMA state + decision),
+// the per-block Gram partials of pass 1, a completion event and (when
+// profiling) four timing events.  A step validates its arguments, enqueues
+// pass1 -> decide -> pass2 on the caller's stream and returns; there is no
+// host synchronisation on the step path and no device-to-host traffic.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "edit_outer_internal.h"
+
+using namespace edit;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+edit_status_t fail(edit_status_t s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+edit_status_t fail_hip(hipError_t e, const char* what) {
+  return fail(EDIT_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+struct Unit {
+  int64_t n = 0;
+  int rows = 1;         // pass-1 blocks = partial rows
+  int blocks2 = 1;      // pass-2 blocks
+  double* partials = nullptr;
+  UnitRecord* rec = nullptr;
+  hipEvent_t done = nullptr;
+  hipEvent_t prof[4] = {nullptr, nullptr, nullptr, nullptr};
+  bool pending = false;   // `done` has been recorded at least once
+  bool profiled = false;  // prof[] hold the last step's timestamps
+  bool has_state = false; // stepped or state_set at least once
+};
+
+}  // namespace
+
+struct edit_outer {
+  edit_outer_config_t cfg{};
+  std::vector<int64_t> numel;
+  int device = 0;
+  int num_cu = 0;
+  int cap1 = 1, cap2 = 1;  // resident blocks of pass 1 / pass 2 on the whole GPU
+  bool profiling = false;
+  char* arena = nullptr;   // one device allocation for every unit's scratch
+  std::vector<Unit> units;
+};
+
+namespace {
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+edit_status_t check_device(const edit_outer* h) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+  if (dev != h->device)
+    return fail(EDIT_EINVAL, "call made with device " + std::to_string(dev) +
+                                 " current; the handle belongs to device " +
+                                 std::to_string(h->device));
+  return EDIT_OK;
+}
+
+void destroy_units(edit_outer* h) {
+  for (Unit& u : h->units) {
+    if (u.done) (void)hipEventDestroy(u.done);
+    for (hipEvent_t& ev : u.prof)
+      if (ev) (void)hipEventDestroy(ev);
+  }
+  h->units.clear();
+  if (h->arena) (void)hipFree(h->arena);
+  h->arena = nullptr;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* edit_outer_strerror(edit_status_t s) {
+  switch (s) {
+    case EDIT_OK: return "ok";
+    case EDIT_EINVAL: return "invalid argument";
+    case EDIT_ENOMEM: return "out of memory";
+    case EDIT_EHIP: return "HIP runtime error";
+    case EDIT_ESTATE: return "invalid state";
+    case EDIT_ENODEV: return "no gfx950 device";
+  }
+  return "unknown status";
+}
+
+const char* edit_outer_last_error(void) { return g_last_error.c_str(); }
+
+edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out) {
+  g_last_error.clear();
+  if (!cfg || !out) return fail(EDIT_EINVAL, "cfg and out must not be NULL");
+  *out = nullptr;
+  const int K = cfg->num_workers;
+  if (K < 1 || K > EDIT_MAX_K)
+    return fail(EDIT_EINVAL, "num_workers must be in 1.." + std::to_string(EDIT_MAX_K));
+  if (cfg->num_layers < 1) return fail(EDIT_EINVAL, "num_layers must be >= 1");
+  if (!cfg->layer_numel) return fail(EDIT_EINVAL, "layer_numel must not be NULL");
+  if (cfg->replica_dtype != EDIT_F32 && cfg->replica_dtype != EDIT_BF16)
+    return fail(EDIT_EINVAL, "replica_dtype must be EDIT_F32 or EDIT_BF16");
+  if (cfg->flags & ~(EDIT_AE | EDIT_WA | EDIT_GC)) return fail(EDIT_EINVAL, "unknown flag bits");
+  if (!(cfg->ema_alpha > 0.0 && cfg->ema_alpha <= 1.0))
+    return fail(EDIT_EINVAL, "ema_alpha must be in (0, 1]");
+  if (!(cfg->clip_eps > 0.0)) return fail(EDIT_EINVAL, "clip_eps must be > 0");
+  if (!(cfg->clip_threshold >= 0.0)) return fail(EDIT_EINVAL, "clip_threshold must be >= 0");
+  if (!std::isfinite(cfg->outer_lr) || !std::isfinite(cfg->momentum) ||
+      !std::isfinite(cfg->z_threshold))
+    return fail(EDIT_EINVAL, "outer_lr, momentum and z_threshold must be finite");
+  if (cfg->ema_warmup_rounds < 0) return fail(EDIT_EINVAL, "ema_warmup_rounds must be >= 0");
+  for (int l = 0; l < cfg->num_layers; ++l)
+    if (cfg->layer_numel[l] < 0)
+      return fail(EDIT_EINVAL, "layer_numel[" + std::to_string(l) + "] is negative");
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+  hipDeviceProp_t prop;
+  e = hipGetDeviceProperties(&prop, dev);
+  if (e != hipSuccess) return fail_hip(e, "hipGetDeviceProperties");
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(EDIT_ENODEV, std::string("device arch is ") + prop.gcnArchName +
+                                 "; this library is built for gfx950 only");
+
+  edit_outer* h = new (std::nothrow) edit_outer;
+  if (!h) return fail(EDIT_ENOMEM, "host allocation failed");
+  h->cfg = *cfg;
+  h->numel.assign(cfg->layer_numel, cfg->layer_numel + cfg->num_layers);
+  h->cfg.layer_numel = h->numel.data();
+  h->device = dev;
+  h->num_cu = prop.multiProcessorCount;
+  const bool bf16 = cfg->replica_dtype == EDIT_BF16;
+  h->cap1 = h->num_cu * pass1_blocks_per_cu(K, bf16);
+  h->cap2 = h->num_cu * pass2_blocks_per_cu(K, bf16);
+
+  // Lay out every unit's record and partials in one allocation.
+  const int ve = bf16 ? 8 : 4;
+  const size_t rec_bytes = (sizeof(UnitRecord) + 255) & ~size_t(255);
+  size_t total = 0;
+  h->units.resize(cfg->num_layers);
+  std::vector<size_t> offs(cfg->num_layers);
+  for (int l = 0; l < cfg->num_layers; ++l) {
+    Unit& u = h->units[l];
+    u.n = h->numel[l];
+    const int64_t nvec = u.n / ve;
+    u.rows = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(h->cap1, ceil_div(nvec, kThreads))));
+    u.blocks2 = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(h->cap2, ceil_div(nvec, kThreads))));
+    offs[l] = total;
+    const size_t part_bytes = (size_t(num_pairs(K)) * u.rows * sizeof(double) + 255) & ~size_t(255);
+    total += rec_bytes + part_bytes;
+  }
+  e = hipMalloc(reinterpret_cast<void**>(&h->arena), total);
+  if (e != hipSuccess) {
+    delete h;
+    return fail(EDIT_ENOMEM, std::string("hipMalloc of scratch: ") + hipGetErrorString(e));
+  }
+  e = hipMemset(h->arena, 0, total);  // EMA state mu = sigma = 0, round 0
+  for (int l = 0; l < cfg->num_layers && e == hipSuccess; ++l) {
+    Unit& u = h->units[l];
+    u.rec = reinterpret_cast<UnitRecord*>(h->arena + offs[l]);
+    u.partials = reinterpret_cast<double*>(h->arena + offs[l] + rec_bytes);
+    e = hipEventCreateWithFlags(&u.done, hipEventDisableTiming);
+  }
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    destroy_units(h);
+    delete h;
+    return fail_hip(e, "init");
+  }
+  *out = h;
+  return EDIT_OK;
+}
+
+edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta, float* momentum,
+                                    void* const* replicas, void* stream) {
+  if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  if (layer < 0 || layer >= h->cfg.num_layers)
+    return fail(EDIT_EINVAL, "layer " + std::to_string(layer) + " out of range");
+  Unit& u = h->units[layer];
+  const int K = h->cfg.num_workers;
+  const bool bf16 = h->cfg.replica_dtype == EDIT_BF16;
+  const int64_t n = u.n;
+  if (!replicas && n > 0) return fail(EDIT_EINVAL, "replicas must not be NULL");
+  if (n > 0) {
+    if (!theta || !momentum) return fail(EDIT_EINVAL, "theta and momentum must not be NULL");
+    if (!aligned16(theta) || !aligned16(momentum))
+      return fail(EDIT_EINVAL, "theta and momentum must be 16-byte aligned");
+    // Every buffer's byte range, for the alias check.
+    struct Range { uintptr_t lo, hi; };
+    Range r[EDIT_MAX_K + 2];
+    r[0] = {reinterpret_cast<uintptr_t>(theta), reinterpret_cast<uintptr_t>(theta) + 4 * n};
+    r[1] = {reinterpret_cast<uintptr_t>(momentum), reinterpret_cast<uintptr_t>(momentum) + 4 * n};
+    const int64_t rb = bf16 ? 2 : 4;
+    for (int j = 0; j < K; ++j) {
+      if (!replicas[j]) return fail(EDIT_EINVAL, "replica pointer " + std::to_string(j) + " is NULL");
+      if (!aligned16(replicas[j]))
+        return fail(EDIT_EINVAL, "replica " + std::to_string(j) + " is not 16-byte aligned");
+      const uintptr_t p = reinterpret_cast<uintptr_t>(replicas[j]);
+      r[2 + j] = {p, p + rb * n};
+    }
+    for (int a = 0; a < K + 2; ++a)
+      for (int b = a + 1; b < K + 2; ++b)
+        if (r[a].lo < r[b].hi && r[b].lo < r[a].hi)
+          return fail(EDIT_EINVAL, "theta, momentum and the replicas must not overlap");
+  }
+  edit_status_t st = check_device(h);
+  if (st != EDIT_OK) return st;
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const void* const* creps = const_cast<const void* const*>(replicas);
+  static void* const kNoReplicas[EDIT_MAX_K] = {};
+  if (n == 0) creps = kNoReplicas;
+  void* const* mreps = n == 0 ? kNoReplicas : replicas;
+
+  DecideParams prm;
+  prm.alpha = h->cfg.ema_alpha;
+  prm.delta = h->cfg.z_threshold;
+  prm.phi = h->cfg.clip_threshold;
+  prm.eps = h->cfg.clip_eps;
+  prm.warmup = h->cfg.ema_warmup_rounds;
+  prm.flags = h->cfg.flags;
+
+  hipError_t e = hipSuccess;
+  const bool prof = h->profiling;
+  if (prof) {
+    for (hipEvent_t& ev : u.prof)
+      if (!ev && (e = hipEventCreate(&ev)) != hipSuccess) return fail_hip(e, "hipEventCreate");
+    if ((e = hipEventRecord(u.prof[0], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+  }
+  e = launch_pass1(K, bf16, u.rows, theta, creps, n, u.partials, s);
+  if (e != hipSuccess) return fail_hip(e, "pass1 launch");
+  if (prof && (e = hipEventRecord(u.prof[1], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+  e = launch_decide(K, u.partials, u.rows, u.rec, prm, s);
+  if (e != hipSuccess) return fail_hip(e, "decide launch");
+  if (prof && (e = hipEventRecord(u.prof[2], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+  e = launch_pass2(K, bf16, u.blocks2, theta, momentum, mreps, u.rec, n,
+                   static_cast<float>(h->cfg.outer_lr), static_cast<float>(h->cfg.momentum), s);
+  if (e != hipSuccess) return fail_hip(e, "pass2 launch");
+  if (prof && (e = hipEventRecord(u.prof[3], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+  if ((e = hipEventRecord(u.done, s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+  u.pending = true;
+  u.profiled = prof;
+  u.has_state = true;
+  return EDIT_OK;
+}
+
+edit_status_t edit_outer_state_get(edit_outer_t h, int32_t layer, edit_layer_state_t* out) {
+  if (!h || !out) return fail(EDIT_EINVAL, "NULL argument");
+  if (layer < 0 || layer >= h->cfg.num_layers)
+    return fail(EDIT_EINVAL, "layer " + std::to_string(layer) + " out of range");
+  Unit& u = h->units[layer];
+  if (!u.has_state) return fail(EDIT_ESTATE, "unit has neither stepped nor had its state set");
+  edit_status_t st = check_device(h);
+  if (st != EDIT_OK) return st;
+  hipError_t e = hipSuccess;
+  if (u.pending && (e = hipEventSynchronize(u.done)) != hipSuccess)
+    return fail_hip(e, "hipEventSynchronize");
+  UnitRecord rec;
+  if ((e = hipMemcpy(&rec, u.rec, sizeof rec, hipMemcpyDeviceToHost)) != hipSuccess)
+    return fail_hip(e, "hipMemcpy D2H");
+  std::memset(out, 0, sizeof *out);
+  const int K = h->cfg.num_workers;
+  out->round = rec.round;
+  out->num_workers = K;
+  out->rolled_back = rec.rollback;
+  out->z_tested = rec.z_tested;
+  for (int j = 0; j < K; ++j) {
+    out->ema_mean[j] = rec.mu[j];
+    out->ema_std[j] = rec.sigma[j];
+    out->norm[j] = rec.norm[j];
+    out->weight[j] = rec.weight[j];
+    out->anomalous[j] = rec.anomalous[j];
+  }
+  out->synced_norm = rec.synced_norm;
+  out->clip_coef = rec.clip_coef;
+  return EDIT_OK;
+}
+
+edit_status_t edit_outer_state_set(edit_outer_t h, int32_t layer, const edit_layer_state_t* in) {
+  if (!h || !in) return fail(EDIT_EINVAL, "NULL argument");
+  if (layer < 0 || layer >= h->cfg.num_layers)
+    return fail(EDIT_EINVAL, "layer " + std::to_string(layer) + " out of range");
+  if (in->round < 0) return fail(EDIT_EINVAL, "round must be >= 0");
+  const int K = h->cfg.num_workers;
+  for (int j = 0; j < K; ++j)
+    if (!std::isfinite(in->ema_mean[j]) || !(in->ema_std[j] >= 0.0) || !std::isfinite(in->ema_std[j]))
+      return fail(EDIT_EINVAL, "EMA state must be finite with ema_std >= 0");
+  Unit& u = h->units[layer];
+  edit_status_t st = check_device(h);
+  if (st != EDIT_OK) return st;
+  hipError_t e = hipSuccess;
+  if (u.pending && (e = hipEventSynchronize(u.done)) != hipSuccess)
+    return fail_hip(e, "hipEventSynchronize");
+  UnitRecord rec;
+  if ((e = hipMemcpy(&rec, u.rec, sizeof rec, hipMemcpyDeviceToHost)) != hipSuccess)
+    return fail_hip(e, "hipMemcpy D2H");
+  for (int j = 0; j < K; ++j) {
+    rec.mu[j] = in->ema_mean[j];
+    rec.sigma[j] = in->ema_std[j];
+  }
+  rec.round = in->round;
+  rec.stepped = 1;
+  if ((e = hipMemcpy(u.rec, &rec, sizeof rec, hipMemcpyHostToDevice)) != hipSuccess)
+    return fail_hip(e, "hipMemcpy H2D");
+  u.has_state = true;
+  return EDIT_OK;
+}
+
+void edit_outer_destroy(edit_outer_t h) {
+  if (!h) return;
+  int prev = -1;
+  if (hipGetDevice(&prev) == hipSuccess && prev != h->device) (void)hipSetDevice(h->device);
+  for (Unit& u : h->units)
+    if (u.pending) (void)hipEventSynchronize(u.done);
+  destroy_units(h);
+  if (prev >= 0 && prev != h->device) (void)hipSetDevice(prev);
+  delete h;
+}
+
+edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t enable) {
+  if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  h->profiling = enable != 0;
+  return EDIT_OK;
+}
+
+edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[3]) {
+  if (!h || !ms) return fail(EDIT_EINVAL, "NULL argument");
+  if (layer < 0 || layer >= h->cfg.num_layers)
+    return fail(EDIT_EINVAL, "layer " + std::to_string(layer) + " out of range");
+  Unit& u = h->units[layer];
+  if (!u.profiled) return fail(EDIT_ESTATE, "the unit's last step was not profiled");
+  hipError_t e = hipEventSynchronize(u.prof[3]);
+  if (e != hipSuccess) return fail_hip(e, "hipEventSynchronize");
+  for (int k = 0; k < 3; ++k)
+    if ((e = hipEventElapsedTime(&ms[k], u.prof[k], u.prof[k + 1])) != hipSuccess)
+      return fail_hip(e, "hipEventElapsedTime");
+  return EDIT_OK;
+}
+
+edit_status_t edit_outer_copy_probe(void* dst, const void* src, int64_t nbytes, void* stream) {
+  if (nbytes < 0 || (nbytes & 15)) return fail(EDIT_EINVAL, "nbytes must be a non-negative multiple of 16");
+  if (nbytes == 0) return EDIT_OK;
+  if (!dst || !src || !aligned16(dst) || !aligned16(src))
+    return fail(EDIT_EINVAL, "dst and src must be non-NULL and 16-byte aligned");
+  const uintptr_t d = reinterpret_cast<uintptr_t>(dst), s = reinterpret_cast<uintptr_t>(src);
+  if (d < s + nbytes && s < d + nbytes) return fail(EDIT_EINVAL, "dst and src overlap");
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return fail_hip(e, "device query");
+  const int64_t nvec = nbytes / 16;
+  const int blocks = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(int64_t(cus) * 8, ceil_div(nvec, kThreads))));
+  e = launch_copy(dst, src, nbytes, blocks, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail_hip(e, "copy launch");
+  return EDIT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,317 @@
+"""Python binding of libedit_outer.so (argument marshalling only).
+
+Every step of the outer synchronization runs in the HIP kernels of the
+library; this module checks tensors, passes device pointers and HIP stream
+handles through the C ABI of include/edit_outer.h, and converts results.
+PyTorch provides the device memory and the streams.  There is no fallback:
+if the library is missing or fails to load, EditOuterError is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import numpy as np
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(PKG, "libedit_outer.so")
+
+MAX_K = 16
+AE, WA, GC = 1, 2, 4
+F32, BF16 = 0, 1
+
+EDIT_OK, EDIT_EINVAL, EDIT_ENOMEM, EDIT_EHIP, EDIT_ESTATE, EDIT_ENODEV = 0, -1, -2, -3, -4, -5
+
+# Every function the header declares; the CPU tests check the library exports them.
+EXPORTS = (
+    "edit_outer_init", "edit_outer_step_layer", "edit_outer_state_get", "edit_outer_state_set",
+    "edit_outer_destroy", "edit_outer_strerror", "edit_outer_last_error",
+    "edit_outer_set_profiling", "edit_outer_kernel_times", "edit_outer_copy_probe",
+)
+
+
+class EditOuterError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [
+        ("num_workers", ctypes.c_int32),
+        ("num_layers", ctypes.c_int32),
+        ("layer_numel", ctypes.POINTER(ctypes.c_int64)),
+        ("replica_dtype", ctypes.c_int32),
+        ("flags", ctypes.c_uint32),
+        ("outer_lr", ctypes.c_double),
+        ("momentum", ctypes.c_double),
+        ("clip_threshold", ctypes.c_double),
+        ("clip_eps", ctypes.c_double),
+        ("ema_alpha", ctypes.c_double),
+        ("z_threshold", ctypes.c_double),
+        ("ema_warmup_rounds", ctypes.c_int64),
+    ]
+
+
+class _LayerState(ctypes.Structure):
+    _fields_ = [
+        ("round", ctypes.c_int64),
+        ("num_workers", ctypes.c_int32),
+        ("rolled_back", ctypes.c_int32),
+        ("z_tested", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+        ("ema_mean", ctypes.c_double * MAX_K),
+        ("ema_std", ctypes.c_double * MAX_K),
+        ("norm", ctypes.c_double * MAX_K),
+        ("weight", ctypes.c_double * MAX_K),
+        ("anomalous", ctypes.c_uint8 * MAX_K),
+        ("synced_norm", ctypes.c_double),
+        ("clip_coef", ctypes.c_double),
+    ]
+
+
+_lib = None
+
+
+def load_library() -> ctypes.CDLL:
+    """Load the in-tree library (built by `python -m paper_2412_07210_amd.build`)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIBRARY):
+        raise EditOuterError(EDIT_ENODEV, f"{LIBRARY} is not built; run "
+                             "`python -m paper_2412_07210_amd.build` (hipcc, gfx950)")
+    lib = ctypes.CDLL(LIBRARY)
+    st = ctypes.c_int
+    vp = ctypes.c_void_p
+    lib.edit_outer_init.argtypes = [ctypes.POINTER(_Config), ctypes.POINTER(vp)]
+    lib.edit_outer_init.restype = st
+    lib.edit_outer_step_layer.argtypes = [vp, ctypes.c_int32, vp, vp, ctypes.POINTER(vp), vp]
+    lib.edit_outer_step_layer.restype = st
+    lib.edit_outer_state_get.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(_LayerState)]
+    lib.edit_outer_state_get.restype = st
+    lib.edit_outer_state_set.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(_LayerState)]
+    lib.edit_outer_state_set.restype = st
+    lib.edit_outer_destroy.argtypes = [vp]
+    lib.edit_outer_destroy.restype = None
+    lib.edit_outer_strerror.argtypes = [st]
+    lib.edit_outer_strerror.restype = ctypes.c_char_p
+    lib.edit_outer_last_error.argtypes = []
+    lib.edit_outer_last_error.restype = ctypes.c_char_p
+    lib.edit_outer_set_profiling.argtypes = [vp, ctypes.c_int32]
+    lib.edit_outer_set_profiling.restype = st
+    lib.edit_outer_kernel_times.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_float)]
+    lib.edit_outer_kernel_times.restype = st
+    lib.edit_outer_copy_probe.argtypes = [vp, vp, ctypes.c_int64, vp]
+    lib.edit_outer_copy_probe.restype = st
+    _lib = lib
+    return lib
+
+
+def _check(status: int, what: str) -> None:
+    if status != EDIT_OK:
+        lib = load_library()
+        msg = lib.edit_outer_last_error().decode(errors="replace")
+        name = lib.edit_outer_strerror(status).decode()
+        raise EditOuterError(status, f"{what}: {name}: {msg}")
+
+
+def _stream_handle(stream: Optional[torch.cuda.Stream], device: torch.device) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return int(s.cuda_stream)
+
+
+@dataclass
+class OuterConfig:
+    """Configuration of one handle; names follow the paper's notation."""
+    num_workers: int                       # K
+    layer_numel: Sequence[int]             # elements of each sync unit
+    replica_dtype: str = "bf16"            # "bf16" or "f32"
+    outer_lr: float = 0.8                  # nu
+    momentum: float = 0.85                 # rho
+    clip_threshold: float = 10.0           # phi (Eq. 4)
+    clip_eps: float = 1e-6                 # eps (Eq. 4)
+    ema_alpha: float = 0.02                # alpha (Eq. 1)
+    z_threshold: float = 3.0               # delta
+    ema_warmup_rounds: int = 10
+    flags: int = AE | WA | GC
+
+    @property
+    def torch_dtype(self) -> torch.dtype:
+        return torch.bfloat16 if self.replica_dtype == "bf16" else torch.float32
+
+
+@dataclass
+class LayerState:
+    round: int
+    rolled_back: bool
+    z_tested: bool
+    ema_mean: np.ndarray
+    ema_std: np.ndarray
+    norm: np.ndarray
+    weight: np.ndarray
+    anomalous: np.ndarray
+    synced_norm: float
+    clip_coef: float
+
+
+class EditOuter:
+    """A handle of the C library: EMA state and scratch for L sync units."""
+
+    def __init__(self, cfg: OuterConfig, device: Optional[torch.device] = None):
+        self.cfg = cfg
+        device = torch.device("cuda") if device is None else torch.device(device)
+        if device.type != "cuda":
+            raise ValueError("the handle needs a GPU device")
+        if device.index is None:
+            device = torch.device("cuda", torch.cuda.current_device())
+        self.device = device
+        if cfg.replica_dtype not in ("bf16", "f32"):
+            raise ValueError("replica_dtype must be 'bf16' or 'f32'")
+        lib = load_library()
+        self._numel = [int(n) for n in cfg.layer_numel]
+        arr = (ctypes.c_int64 * len(self._numel))(*self._numel)
+        c = _Config(int(cfg.num_workers), len(self._numel), arr,
+                    BF16 if cfg.replica_dtype == "bf16" else F32, int(cfg.flags),
+                    float(cfg.outer_lr), float(cfg.momentum), float(cfg.clip_threshold),
+                    float(cfg.clip_eps), float(cfg.ema_alpha), float(cfg.z_threshold),
+                    int(cfg.ema_warmup_rounds))
+        h = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            _check(lib.edit_outer_init(ctypes.byref(c), ctypes.byref(h)), "edit_outer_init")
+        self._h = h
+        self._lib = lib
+
+    # -- lifetime ------------------------------------------------------------
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            with torch.cuda.device(self.device):
+                self._lib.edit_outer_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    # -- the step --------------------------------------------------------------
+    def _check_tensor(self, t: torch.Tensor, n: int, dtype: torch.dtype, what: str) -> None:
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{what} must be a torch.Tensor")
+        if t.device != self.device:
+            raise ValueError(f"{what} is on {t.device}, the handle on {self.device}")
+        if t.dtype != dtype:
+            raise ValueError(f"{what} must be {dtype}, got {t.dtype}")
+        if not t.is_contiguous():
+            raise ValueError(f"{what} must be contiguous")
+        if t.numel() != n:
+            raise ValueError(f"{what} has {t.numel()} elements, unit has {n}")
+
+    def step_layer(self, layer: int, theta: torch.Tensor, momentum: torch.Tensor,
+                   replicas: Sequence[torch.Tensor], stream: Optional[torch.cuda.Stream] = None) -> None:
+        """Enqueue one outer step of unit `layer` (in place on all tensors)."""
+        if not 0 <= layer < len(self._numel):
+            raise IndexError(f"layer {layer} out of range")
+        n = self._numel[layer]
+        K = self.cfg.num_workers
+        if len(replicas) != K:
+            raise ValueError(f"expected {K} replicas, got {len(replicas)}")
+        self._check_tensor(theta, n, torch.float32, "theta")
+        self._check_tensor(momentum, n, torch.float32, "momentum")
+        for j, r in enumerate(replicas):
+            self._check_tensor(r, n, self.cfg.torch_dtype, f"replicas[{j}]")
+        ptrs = (ctypes.c_void_p * K)(*[r.data_ptr() for r in replicas])
+        if torch.cuda.current_device() != self.device.index:
+            with torch.cuda.device(self.device):
+                status = self._lib.edit_outer_step_layer(self._h, int(layer), theta.data_ptr(),
+                                                         momentum.data_ptr(), ptrs,
+                                                         _stream_handle(stream, self.device))
+        else:
+            status = self._lib.edit_outer_step_layer(self._h, int(layer), theta.data_ptr(),
+                                                     momentum.data_ptr(), ptrs,
+                                                     _stream_handle(stream, self.device))
+        _check(status, "edit_outer_step_layer")
+
+    def step_round(self, units: Sequence[tuple], streams: Optional[List[torch.cuda.Stream]] = None,
+                   layers: Optional[Sequence[int]] = None) -> None:
+        """Step every unit in forward order; unit l goes to streams[l % S].
+
+        units[l] = (theta, momentum, replicas).  The streams start after the
+        current stream's pending work and the current stream waits for all of
+        them, so the round is ordered like a single call on the current stream.
+        """
+        cur = torch.cuda.current_stream(self.device)
+        layers = list(range(len(units))) if layers is None else list(layers)
+        if not streams:
+            for l, (th, b, reps) in zip(layers, units):
+                self.step_layer(l, th, b, reps, stream=cur)
+            return
+        start = torch.cuda.Event()
+        start.record(cur)
+        for s in streams:
+            s.wait_event(start)
+        for i, (l, (th, b, reps)) in enumerate(zip(layers, units)):
+            self.step_layer(l, th, b, reps, stream=streams[i % len(streams)])
+        for s in streams:
+            ev = torch.cuda.Event()
+            ev.record(s)
+            cur.wait_event(ev)
+
+    # -- state ----------------------------------------------------------------
+    def state_get(self, layer: int) -> LayerState:
+        st = _LayerState()
+        with torch.cuda.device(self.device):
+            _check(self._lib.edit_outer_state_get(self._h, int(layer), ctypes.byref(st)),
+                   "edit_outer_state_get")
+        K = self.cfg.num_workers
+        return LayerState(
+            round=int(st.round), rolled_back=bool(st.rolled_back), z_tested=bool(st.z_tested),
+            ema_mean=np.array(st.ema_mean[:K]), ema_std=np.array(st.ema_std[:K]),
+            norm=np.array(st.norm[:K]), weight=np.array(st.weight[:K]),
+            anomalous=np.array(st.anomalous[:K], dtype=np.uint8),
+            synced_norm=float(st.synced_norm), clip_coef=float(st.clip_coef))
+
+    def state_set(self, layer: int, ema_mean: Sequence[float], ema_std: Sequence[float],
+                  round_: int) -> None:
+        st = _LayerState()
+        st.round = int(round_)
+        st.num_workers = self.cfg.num_workers
+        for j in range(self.cfg.num_workers):
+            st.ema_mean[j] = float(ema_mean[j])
+            st.ema_std[j] = float(ema_std[j])
+        with torch.cuda.device(self.device):
+            _check(self._lib.edit_outer_state_set(self._h, int(layer), ctypes.byref(st)),
+                   "edit_outer_state_set")
+
+    # -- measurement ------------------------------------------------------------
+    def set_profiling(self, enable: bool) -> None:
+        _check(self._lib.edit_outer_set_profiling(self._h, int(bool(enable))), "set_profiling")
+
+    def kernel_times(self, layer: int) -> tuple:
+        """(pass1 ms, decide ms, pass2 ms) of the unit's last profiled step."""
+        ms = (ctypes.c_float * 3)()
+        with torch.cuda.device(self.device):
+            _check(self._lib.edit_outer_kernel_times(self._h, int(layer), ms), "kernel_times")
+        return float(ms[0]), float(ms[1]), float(ms[2])
+
+
+def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Plain device copy kernel of the library (bandwidth / counter calibration)."""
+    if dst.device != src.device or dst.device.type != "cuda":
+        raise ValueError("dst and src must be on the same GPU")
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("dst and src sizes differ")
+    lib = load_library()
+    _check(lib.edit_outer_copy_probe(dst.data_ptr(), src.data_ptr(), nbytes,
+                                     _stream_handle(stream, dst.device)), "edit_outer_copy_probe")

@@ -1,0 +1,202 @@
+"""GPU-vs-oracle parity harness (test code; also used by the smoke check).
+
+Each round, both sides receive byte-identical inputs: theta_t and b_t are the
+ORACLE's outputs of the previous round (copied to the device), and the
+replicas are made on the device by the seeded generator from that theta_t
+and copied back to the host.  The EMA state evolves independently on each
+side.  Outputs are compared after every round:
+
+  * anomaly mask and rollback flag: exact, except decisions the oracle
+    reports within 1e-5 (relative) of the z-test threshold, where rounding
+    may legitimately decide either way (those stop the comparison of that
+    unit and are reported as near ties);
+  * G, mu, sigma, w, Gbar, beta: relative 1e-5;
+  * theta, b (fp32): |gpu - oracle| <= 1e-5 * (|oracle| + rms(oracle)) elementwise;
+  * bf16 replicas: every element within one bf16 ulp of the oracle's value and
+    ||gpu - oracle|| / ||oracle|| <= 2e-3; fp32 replicas as theta.
+"""
+from __future__ import annotations
+
+import math
+import time
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from oracle import OracleConfig, OracleUnit
+from paper_2412_07210_amd import EditOuter, OuterConfig
+from paper_2412_07210_amd.synth import Workload
+
+NEAR_TIE = 1e-5
+RTOL_SCALAR = 1e-5
+RTOL_F32 = 1e-5
+BF16_REL_NORM = 2e-3
+
+
+class NearTie(Exception):
+    pass
+
+
+def host_bits(t: torch.Tensor) -> np.ndarray:
+    """Device tensor -> host numpy (bf16 as uint16 bit patterns)."""
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+def bf16_to_f32(h: np.ndarray) -> np.ndarray:
+    return (h.astype(np.uint32) << 16).view(np.float32)
+
+
+def bf16_ulp(x: np.ndarray) -> np.ndarray:
+    _, e = np.frexp(np.abs(x.astype(np.float64)))
+    ulp = np.ldexp(1.0, e - 8)
+    return np.where(x == 0, np.ldexp(1.0, -133), ulp)
+
+
+def assert_tensor_close(gpu: np.ndarray, ref: np.ndarray, what: str) -> None:
+    g = gpu.astype(np.float64)
+    r = ref.astype(np.float64)
+    assert np.all(np.isfinite(g)) == np.all(np.isfinite(r)), f"{what}: non-finite mismatch"
+    rms = math.sqrt(float(np.mean(r * r))) if r.size else 0.0
+    tol = RTOL_F32 * (np.abs(r) + rms)
+    err = np.abs(g - r)
+    bad = err > tol
+    if bad.any():
+        i = int(np.argmax(err - tol))
+        raise AssertionError(f"{what}: {int(bad.sum())} of {r.size} elements out of tolerance; "
+                             f"worst at {i}: gpu {g[i]!r} oracle {r[i]!r} tol {tol[i]:.3e}")
+
+
+def assert_replica_close(gpu: np.ndarray, ref: np.ndarray, bf16: bool, what: str) -> None:
+    if not bf16:
+        assert_tensor_close(gpu, ref, what)
+        return
+    g, r = bf16_to_f32(gpu).astype(np.float64), bf16_to_f32(ref).astype(np.float64)
+    err = np.abs(g - r)
+    bad = err > bf16_ulp(r)
+    if bad.any():
+        i = int(np.argmax(err - bf16_ulp(r)))
+        raise AssertionError(f"{what}: {int(bad.sum())} elements differ by more than one bf16 ulp; "
+                             f"worst at {i}: gpu {g[i]!r} oracle {r[i]!r}")
+    nr = float(np.linalg.norm(r))
+    if nr > 0:
+        rel = float(np.linalg.norm(g - r)) / nr
+        assert rel <= BF16_REL_NORM, f"{what}: relative norm error {rel:.3e}"
+
+
+def assert_scalars(gpu, ref, what, rtol=RTOL_SCALAR):
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    ok = np.isclose(gpu, ref, rtol=rtol, atol=1e-300) | (np.isnan(gpu) & np.isnan(ref)) | (gpu == ref)
+    assert ok.all(), f"{what}: gpu {gpu} oracle {ref}"
+
+
+def compare_decision(st, rec, K: int, what: str) -> None:
+    """Compare the library's LayerState with the oracle record of the same round."""
+    mask_g = np.asarray(st.anomalous[:K], dtype=np.uint8)
+    mask_o = np.asarray(rec["anomalous"][:K], dtype=np.uint8)
+    near = np.asarray(rec["margin"][:K]) < NEAR_TIE
+    if np.any(mask_g[near] != mask_o[near]):
+        raise NearTie(f"{what}: near-tie z-test decision (margin < {NEAR_TIE}); "
+                      "mask parity unpinned for this decision")
+    assert np.array_equal(mask_g, mask_o), f"{what}: mask gpu {mask_g} oracle {mask_o}"
+    assert int(st.rolled_back) == rec["rolled_back"], f"{what}: rollback differs"
+    assert int(st.z_tested) == rec["z_tested"], f"{what}: z_tested differs"
+    assert st.round == rec["round"], f"{what}: round {st.round} vs {rec['round']}"
+    fin = np.isfinite(rec["norm"][:K])
+    assert_scalars(np.asarray(st.norm[:K])[fin], rec["norm"][:K][fin], f"{what}: G")
+    assert_scalars(st.ema_mean[:K], rec["mu"][:K], f"{what}: mu")
+    assert_scalars(st.ema_std[:K], rec["sigma"][:K], f"{what}: sigma")
+    assert_scalars(st.weight[:K], rec["weight"][:K], f"{what}: w")
+    if not rec["rolled_back"]:
+        # Gbar comes from the Gram identity on the GPU and from the
+        # materialised average in the oracle; relative to the largest norm.
+        scale = max(float(np.max(rec["norm"][:K][fin], initial=0.0)), 1e-300)
+        assert abs(st.synced_norm - rec["synced_norm"]) <= RTOL_SCALAR * max(rec["synced_norm"], 1e-3 * scale), \
+            f"{what}: Gbar gpu {st.synced_norm} oracle {rec['synced_norm']}"
+        assert_scalars(st.clip_coef, rec["clip_coef"], f"{what}: beta")
+
+
+@dataclass
+class UnitCase:
+    unit: int
+    oracle: OracleUnit
+    theta_h: np.ndarray
+    mom_h: np.ndarray
+    theta_d: torch.Tensor
+    mom_d: torch.Tensor
+    reps_d: List[torch.Tensor]
+    records: List[dict] = field(default_factory=list)
+
+
+class ParityRun:
+    """Lock-step GPU library vs CPU oracle over selected units of a workload.
+
+    The library handle is created for *all* units of the workload (so each
+    unit's launch configuration is the one the benchmark uses), and only the
+    selected units are stepped.
+    """
+
+    def __init__(self, wl: Workload, units: Sequence[int], device="cuda", seed: int = 0,
+                 flags: Optional[int] = None, ema_state: Optional[Dict[int, tuple]] = None,
+                 handle_units: str = "all"):
+        self.wl, self.seed, self.device = wl, seed, torch.device(device)
+        hyper = wl.hyper()
+        kw = {} if flags is None else {"flags": flags}
+        numel = wl.layer_numel if handle_units == "all" else [wl.unit_numel(u) for u in units]
+        self.index = {u: (u if handle_units == "all" else i) for i, u in enumerate(units)}
+        self.lib = EditOuter(OuterConfig(num_workers=wl.num_workers, layer_numel=numel,
+                                         replica_dtype=wl.replica_dtype,
+                                         ema_warmup_rounds=hyper.pop("warmup_rounds"), **hyper, **kw),
+                             device=self.device)
+        ocfg = OracleConfig(**wl.hyper(), **kw)
+        self.cases: List[UnitCase] = []
+        for u in units:
+            th = wl.init_theta(u, self.device, seed)
+            case = UnitCase(u, OracleUnit(wl.num_workers, ocfg), th.cpu().numpy().copy(),
+                            np.zeros(th.numel(), np.float32), th, torch.zeros_like(th),
+                            [torch.empty(th.numel(), dtype=wl.torch_dtype, device=self.device)
+                             for _ in range(wl.num_workers)])
+            if ema_state and u in ema_state:
+                mu, sig, r = ema_state[u]
+                case.oracle.set_state(mu, sig, r)
+                self.lib.state_set(self.index[u], mu, sig, r)
+            self.cases.append(case)
+
+    def round(self, t: int, std: Optional[np.ndarray] = None, poison: Optional[dict] = None,
+              verbose: bool = False) -> List[dict]:
+        """One outer round on every selected unit; returns the oracle records."""
+        out = []
+        for c in self.cases:
+            t0 = time.time()
+            c.theta_d.copy_(torch.from_numpy(c.theta_h))
+            c.mom_d.copy_(torch.from_numpy(c.mom_h))
+            self.wl.fill_replicas(c.theta_d, c.reps_d, c.unit, t, self.seed, std=std)
+            if poison:
+                for j, (idx, val) in poison.items():
+                    c.reps_d[j][idx] = val
+            reps_h = [host_bits(r) for r in c.reps_d]
+            self.lib.step_layer(self.index[c.unit], c.theta_d, c.mom_d, c.reps_d)
+            rec = c.oracle.step(c.theta_h, c.mom_h, reps_h)
+            torch.cuda.synchronize(self.device)
+            what = f"{self.wl.name} unit {c.unit} round {t}"
+            st = self.lib.state_get(self.index[c.unit])
+            compare_decision(st, rec, self.wl.num_workers, what)
+            assert_tensor_close(c.theta_d.cpu().numpy(), c.theta_h, what + ": theta")
+            assert_tensor_close(c.mom_d.cpu().numpy(), c.mom_h, what + ": momentum")
+            bf16 = self.wl.replica_dtype == "bf16"
+            for j, r in enumerate(c.reps_d):
+                assert_replica_close(host_bits(r), reps_h[j], bf16, what + f": replica {j}")
+            rec = dict(rec, state=st)
+            c.records.append(rec)
+            out.append(rec)
+            if verbose:
+                print(f"  {what}: mask {list(rec['anomalous'])} beta {rec['clip_coef']:.4f} "
+                      f"rolled_back {rec['rolled_back']} ({time.time() - t0:.1f}s)", flush=True)
+        return out
+
+    def close(self):
+        self.lib.close()

@@ -1,0 +1,273 @@
+"""GPU parity of the HIP outer step against the CPU oracle (needs an MI355X).
+
+Small cases span several 256-thread blocks and ragged tails; full-size
+cases run single units of each workload at their real shapes, through a
+handle configured with every unit of the workload, i.e. the launch
+configuration the benchmark times.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from parity import NearTie, ParityRun, host_bits
+from paper_2412_07210_amd import AE, GC, WA, EditOuter, EditOuterError, OuterConfig
+from paper_2412_07210_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _run(run: ParityRun, rounds, verbose=True, **kw):
+    try:
+        recs = []
+        for t in rounds:
+            recs.append(run.round(t, verbose=verbose, **kw))
+        return recs
+    except NearTie as e:
+        pytest.skip(str(e))
+    finally:
+        run.close()
+
+
+def _expected_ema(wl, u, round_, seed=0):
+    """A plausible EMA state (same on both sides) to start a full-size case
+    after the warm-up without paying for the warm-up rounds."""
+    G = wl.delta_std * math.sqrt(wl.unit_numel(u))
+    K = wl.num_workers
+    return (np.full(K, 1.25 * G), np.full(K, 0.45 * G), round_)
+
+
+# ------------------------------------------------------------------ C1
+
+
+def test_c1_linear_layer_all_rounds():
+    """1024x1024 fp32, K = 4: ten clean rounds, then worker 3 x50 is masked."""
+    wl = synth.get("c1")
+    run = ParityRun(wl, [0], DEV)
+    recs = _run(run, range(11))
+    assert [int(x) for x in recs[10][0]["anomalous"]] == [0, 0, 0, 1]
+    assert all(not r[0]["anomalous"].any() for r in recs[:10])
+    assert recs[10][0]["clip_coef"] == 1.0
+
+
+# ----------------------------------------------------- small and ragged
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("K", [1, 2, 3, 5, 8, 13, 16])
+def test_ragged_sizes(K, dtype):
+    """Unit sizes around the 16-byte vector and the 256-thread block, K = 1..16."""
+    sizes = [0, 1, 7, 8, 9, 255, 2049, 100_003, 1_000_005]
+    wl = synth.small("c3", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=2,
+                     clip_threshold=0.05, name=f"ragged{K}{dtype}")
+    run = ParityRun(wl, range(len(sizes)), DEV)
+    std = lambda t: wl.worker_std(t) * (np.where(np.arange(K) == K - 1, 40.0, 1.0) if t == 3 else 1.0)
+    try:
+        for t in range(4):
+            run.round(t, std=std(t), verbose=False)
+    except NearTie as e:
+        pytest.skip(str(e))
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("flags", range(8))
+def test_flag_combinations(flags):
+    """Every on/off combination of anomaly elimination, weighting and clipping
+    (flags = 0 is the DiLoCo outer step)."""
+    wl = synth.small("c3", [300_001, 4096], num_workers=4, warmup_rounds=2, clip_threshold=0.2,
+                     name="flags")
+    run = ParityRun(wl, [0, 1], DEV, flags=flags)
+    K = wl.num_workers
+    try:
+        for t in range(4):
+            std = wl.worker_std(t)
+            if t == 3:
+                std[1] *= 50
+            run.round(t, std=std, verbose=False)
+    except NearTie as e:
+        pytest.skip(str(e))
+    finally:
+        run.close()
+
+
+def test_rollback_when_all_workers_flagged():
+    """Every worker x100 after the warm-up: theta and b keep their values,
+    all replicas get theta_t back (Sec. 3.2, Algorithm 2)."""
+    wl = synth.small("c3", [65_536 + 3], num_workers=4, warmup_rounds=2, name="rollback")
+    run = ParityRun(wl, [0], DEV)
+    try:
+        for t in range(2):
+            run.round(t)
+        c = run.cases[0]
+        theta_before = c.theta_h.copy()
+        mom_before = c.mom_h.copy()
+        recs = run.round(2, std=wl.worker_std(2) * 100)
+        assert recs[0]["rolled_back"] == 1
+        assert np.array_equal(c.theta_d.cpu().numpy(), theta_before)
+        assert np.array_equal(c.mom_d.cpu().numpy(), mom_before)
+        st = recs[0]["state"]
+        assert st.rolled_back and st.anomalous.all() and st.clip_coef == 0.0
+    finally:
+        run.close()
+
+
+def test_nonfinite_worker_is_masked():
+    """A NaN in one replica makes its norm non-finite: that worker is masked
+    (even during the warm-up) and the others still synchronize."""
+    wl = synth.small("c3", [10_000, 77], num_workers=5, warmup_rounds=5, name="nan")
+    run = ParityRun(wl, [0, 1], DEV)
+    try:
+        recs = run.round(0, poison={2: (13, float("nan"))})
+        for r in recs:
+            assert list(r["anomalous"]) == [0, 0, 1, 0, 0]
+            assert np.isfinite(run.cases[0].theta_d.cpu().numpy()).all()
+        run.round(1, poison={0: (5, float("inf"))})
+    finally:
+        run.close()
+
+
+# ------------------------------------------------------------ full size
+
+
+def test_c2_full_units():
+    """Llama-350M-shaped units (12,847,104 fp32 elements, K = 8)."""
+    wl = synth.get("c2")
+    units = [0, 23]
+    run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 10) for u in units})
+    _run(run, [10, 11])
+
+
+def test_c3_full_units_with_anomaly():
+    """Llama-1B-shaped units (51,384,320 elements, bf16 replicas, K = 8),
+    rounds 18-19: round 19 has one worker x20, which must be masked."""
+    wl = synth.get("c3")
+    units = [0, 11]
+    run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 18) for u in units})
+    recs = _run(run, [18, 19])
+    bad = list(wl.anomalies(19).keys())[0]
+    for r in recs[1]:
+        assert r["anomalous"][bad] == 1
+
+
+def test_c4_full_unit_clip_active():
+    """7B half shard (101,191,680 elements, bf16, K = 8) with phi = 0.889: clipping active."""
+    wl = synth.get("c4")
+    run = ParityRun(wl, [5], DEV, ema_state={5: _expected_ema(wl, 5, 10)})
+    recs = _run(run, [10])
+    assert recs[0][0]["clip_coef"] < 1.0
+
+
+def test_c5_full_layer_k16():
+    """A-EDiT round on 1B shapes, K = 16: one layer's matrix unit (51,380,224)
+    and its two 2,048-element RMSNorm units, three workers x30."""
+    wl = synth.get("c5")
+    units = [0, 1, 2]
+    run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 10) for u in units})
+    recs = _run(run, [10])
+    flagged = sorted(wl.anomalies(10).keys())
+    for r in recs[0]:
+        assert sorted(np.flatnonzero(r["anomalous"]).tolist()) == flagged
+
+
+# ------------------------------------------------- determinism, resume
+
+
+def _fresh_inputs(wl, u, t, dev):
+    th = wl.init_theta(u, dev)
+    reps = [torch.empty(th.numel(), dtype=wl.torch_dtype, device=dev) for _ in range(wl.num_workers)]
+    wl.fill_replicas(th, reps, u, t)
+    return th, torch.zeros_like(th), reps
+
+
+def test_bitwise_deterministic():
+    wl = synth.small("c3", [3_000_017], name="det")
+    outs = []
+    for _ in range(2):
+        h = EditOuter(OuterConfig(wl.num_workers, wl.layer_numel, "bf16"), DEV)
+        th, b, reps = _fresh_inputs(wl, 0, 0, DEV)
+        h.step_layer(0, th, b, reps)
+        torch.cuda.synchronize()
+        outs.append((th.clone(), b.clone(), [r.clone() for r in reps], h.state_get(0)))
+        h.close()
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+    assert all(torch.equal(a, b) for a, b in zip(outs[0][2], outs[1][2]))
+    assert np.array_equal(outs[0][3].norm, outs[1][3].norm)
+
+
+def test_resume_from_saved_state_is_bitwise():
+    """20 rounds straight equal 10 rounds, save EMA state, new handle, restore, 10 rounds."""
+    wl = synth.small("c3", [200_003], warmup_rounds=4, name="resume")
+    cfg = OuterConfig(wl.num_workers, wl.layer_numel, "bf16", ema_warmup_rounds=4)
+
+    def play(h, th, b, reps, rounds, h_switch=None):
+        for t in rounds:
+            wl.fill_replicas(th, reps, 0, t)
+            h.step_layer(0, th, b, reps)
+        torch.cuda.synchronize()
+
+    th, b, reps = _fresh_inputs(wl, 0, 0, DEV)
+    th2, b2, reps2 = th.clone(), b.clone(), [r.clone() for r in reps]
+    a = EditOuter(cfg, DEV)
+    play(a, th, b, reps, range(20))
+    s1 = EditOuter(cfg, DEV)
+    play(s1, th2, b2, reps2, range(10))
+    st = s1.state_get(0)
+    s1.close()
+    s2 = EditOuter(cfg, DEV)
+    s2.state_set(0, st.ema_mean, st.ema_std, st.round)
+    play(s2, th2, b2, reps2, range(10, 20))
+    assert torch.equal(th, th2) and torch.equal(b, b2)
+    sa, sb = a.state_get(0), s2.state_get(0)
+    assert sa.round == sb.round == 20
+    assert np.array_equal(sa.ema_mean, sb.ema_mean) and np.array_equal(sa.ema_std, sb.ema_std)
+    a.close()
+    s2.close()
+
+
+def test_stream_pipeline_matches_single_stream():
+    """Units issued in forward order over three streams give the same bits as
+    issuing them on one stream."""
+    wl = synth.small("c3", [1_000_000 + 8 * i for i in range(6)], name="pipe")
+    results = []
+    for streams in (None, [torch.cuda.Stream() for _ in range(3)]):
+        h = EditOuter(OuterConfig(wl.num_workers, wl.layer_numel, "bf16"), DEV)
+        units = [_fresh_inputs(wl, u, 0, DEV) for u in range(wl.num_units)]
+        torch.cuda.synchronize()
+        h.step_round(units, streams=streams)
+        torch.cuda.synchronize()
+        results.append(units)
+        h.close()
+    for (a, b) in zip(*results):
+        assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+        assert all(torch.equal(x, y) for x, y in zip(a[2], b[2]))
+
+
+# ------------------------------------------------------------ API errors
+
+
+def test_step_rejects_bad_arguments():
+    wl = synth.small("c3", [4096, 100], name="api")
+    h = EditOuter(OuterConfig(wl.num_workers, wl.layer_numel, "bf16"), DEV)
+    th, b, reps = _fresh_inputs(wl, 0, 0, DEV)
+    with pytest.raises(IndexError):
+        h.step_layer(2, th, b, reps)
+    with pytest.raises(ValueError):
+        h.step_layer(0, th, b, reps[:-1])
+    with pytest.raises(ValueError):
+        h.step_layer(0, th, b.double(), reps)
+    # misaligned pointer (offset by one element) is refused by the library
+    big = torch.zeros(4097, dtype=torch.float32, device=DEV)
+    with pytest.raises(EditOuterError) as e:
+        h.step_layer(0, big[1:], b, reps)
+    assert "aligned" in str(e.value)
+    # aliasing replicas are refused
+    with pytest.raises(EditOuterError) as e:
+        h.step_layer(0, th, b, [reps[0]] * wl.num_workers)
+    assert "overlap" in str(e.value)
+    with pytest.raises(EditOuterError):
+        h.state_get(1)  # never stepped
+    h.close()
