@@ -23,7 +23,7 @@ struct alignas(16) UnitRecord {
   double synced_norm;       // ||Delta_bar||
   double clip_coef;         // beta
   int64_t round;            // completed rounds of this unit
-  float coef[kMaxK];        // beta * w_j in fp32, consumed by the update pass
+  double coef[kMaxK];       // beta * w_j, consumed by the update pass
   int32_t src[kMaxK];       // worker whose data the update pass loads for slot j
   int32_t rollback;         // 1: every worker flagged, reset replicas only
   int32_t use_deltas;       // 0: no worker has a non-zero coefficient
@@ -46,8 +46,8 @@ hipError_t launch_pass1(int K, bool bf16, int blocks, const float* theta,
 hipError_t launch_decide(int K, const double* partials, int rows, UnitRecord* rec,
                          const DecideParams& prm, hipStream_t stream);
 hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom,
-                        void* const* reps, const UnitRecord* rec, int64_t n, float lr,
-                        float rho, hipStream_t stream);
+                        void* const* reps, const UnitRecord* rec, int64_t n, double lr,
+                        double rho, hipStream_t stream);
 hipError_t launch_copy(void* dst, const void* src, int64_t nbytes, int blocks,
                        hipStream_t stream);
 

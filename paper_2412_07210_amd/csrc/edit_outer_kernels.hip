@@ -16,6 +16,9 @@
 //          coefficient, forms Delta_hat = sum_j beta w_j Delta_j (Eq. 3, 5),
 //          applies Nesterov momentum and writes theta, b and all K replicas.
 //
+// Storage is fp32 (theta, b) and fp32/bf16 (replicas); arithmetic is fp64
+// from the exact pseudo gradients on, rounded once when stored.
+//
 // The passes are HBM-bound (about 2-3 flop per byte at K = 8), so there is
 // no MFMA: each lane moves 16-byte vectors (global_load_dwordx4), the grid is
 // persistent (resident blocks only, grid-stride over 16-byte vectors) so the
@@ -125,6 +128,14 @@ __device__ __forceinline__ double wave_sum(double x) {
 
 // ---------------------------------------------------------------- pass 1
 
+// Element e of a 16-byte replica vector minus theta, in fp64: the pseudo
+// gradient of that element, exact for every pair of fp32/bf16 inputs whose
+// exponents differ by less than 29.
+template <bool BF16>
+__device__ __forceinline__ double delta64(const uint4& raw, int e, float th) {
+  return static_cast<double>(element<BF16>(raw, e)) - static_cast<double>(th);
+}
+
 template <int K, bool BF16>
 __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __restrict__ theta,
                                                               ConstPtrs<K> reps, int64_t nvec,
@@ -132,14 +143,13 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
                                                               double* __restrict__ partials) {
   constexpr int NP = K * (K + 1) / 2;
   constexpr int VE = Vec<BF16>::VE;
-  // K <= 8: fp32 products of one vector, then fp64 running sums.
-  // K > 8: fp32 running sums (136 fp64 accumulators would not fit).
-  constexpr bool kWide = K <= 8;
-  using Acc = std::conditional_t<kWide, double, float>;
-
-  Acc acc[NP];
+  // fp64 products and sums: on CDNA3/4 a v_fma_f64 issues at the rate of an
+  // unpacked v_fma_f32, so exactness costs no extra VALU cycles, and the
+  // Gram identity for ||sum_j w_j Delta_j|| stays accurate even when the
+  // workers' pseudo gradients nearly cancel.
+  double acc[NP];
 #pragma unroll
-  for (int p = 0; p < NP; ++p) acc[p] = Acc(0);
+  for (int p = 0; p < NP; ++p) acc[p] = 0.0;
 
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
   for (int64_t v = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; v < nvec; v += stride) {
@@ -148,50 +158,31 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
     uint4 raw[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) raw[j] = reinterpret_cast<const uint4*>(reps.p[j])[v];
-
-    if constexpr (kWide) {
-      float part[NP];
 #pragma unroll
-      for (int p = 0; p < NP; ++p) part[p] = 0.f;
+    for (int e = 0; e < VE; ++e) {
+      double d[K];
 #pragma unroll
-      for (int e = 0; e < VE; ++e) {
-        float d[K];
+      for (int j = 0; j < K; ++j) d[j] = delta64<BF16>(raw[j], e, th[e]);
+      int p = 0;
 #pragma unroll
-        for (int j = 0; j < K; ++j) d[j] = element<BF16>(raw[j], e) - th[e];
-        int p = 0;
+      for (int j = 0; j < K; ++j)
 #pragma unroll
-        for (int j = 0; j < K; ++j)
-#pragma unroll
-          for (int k = j; k < K; ++k, ++p) part[p] = fmaf(d[j], d[k], part[p]);
-      }
-#pragma unroll
-      for (int p = 0; p < NP; ++p) acc[p] += static_cast<double>(part[p]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < VE; ++e) {
-        float d[K];
-#pragma unroll
-        for (int j = 0; j < K; ++j) d[j] = element<BF16>(raw[j], e) - th[e];
-        int p = 0;
-#pragma unroll
-        for (int j = 0; j < K; ++j)
-#pragma unroll
-          for (int k = j; k < K; ++k, ++p) acc[p] = fmaf(d[j], d[k], acc[p]);
-      }
+        for (int k = j; k < K; ++k, ++p) acc[p] = fma(d[j], d[k], acc[p]);
     }
   }
 
   // Ragged tail (fewer than VE elements past the last full vector): block 0.
   const int64_t i = nvec * VE + threadIdx.x;
   if (blockIdx.x == 0 && i < n) {
-    float d[K];
+    double d[K];
+    const double th = theta[i];
 #pragma unroll
-    for (int j = 0; j < K; ++j) d[j] = load_scalar<BF16>(reps.p[j], i) - theta[i];
+    for (int j = 0; j < K; ++j) d[j] = static_cast<double>(load_scalar<BF16>(reps.p[j], i)) - th;
     int p = 0;
 #pragma unroll
     for (int j = 0; j < K; ++j)
 #pragma unroll
-      for (int k = j; k < K; ++k, ++p) acc[p] += static_cast<Acc>(d[j] * d[k]);
+      for (int k = j; k < K; ++k, ++p) acc[p] = fma(d[j], d[k], acc[p]);
   }
 
   // Block reduction: wave butterfly, then the four waves in order.
@@ -200,7 +191,7 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
   const int wave = threadIdx.x >> 6;
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
-    const double s = wave_sum(static_cast<double>(acc[p]));
+    const double s = wave_sum(acc[p]);
     if (lane == 0) red[wave][p] = s;
   }
   __syncthreads();
@@ -313,16 +304,16 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const double* __restri
   int first = -1;
 #pragma unroll
   for (int j = 0; j < K; ++j) {
-    const float c = static_cast<float>(beta * w[j]);
+    const double c = beta * w[j];
     rec->weight[j] = w[j];
     rec->coef[j] = c;
-    if (c != 0.f && first < 0) first = j;
+    if (c != 0.0 && first < 0) first = j;
   }
   // The update pass loads slot j from worker src[j]: itself when it
   // contributes, otherwise a contributing worker (a cache hit, and never the
   // data of a flagged worker, which may hold NaN).
 #pragma unroll
-  for (int j = 0; j < K; ++j) rec->src[j] = (rec->coef[j] != 0.f || first < 0) ? j : first;
+  for (int j = 0; j < K; ++j) rec->src[j] = (rec->coef[j] != 0.0 || first < 0) ? j : first;
   rec->use_deltas = first >= 0 ? 1 : 0;
   rec->rollback = n_ok == 0 ? 1 : 0;
   rec->synced_norm = gbar;
@@ -334,13 +325,24 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const double* __restri
 
 // ---------------------------------------------------------------- pass 2
 
+// theta' and b' of one element, in fp64 from fp32 inputs (rounded once on store):
+//   Delta_hat = sum_j c_j (r_j - theta), c_j = beta w_j      (Eq. 3, 5)
+//   g = -Delta_hat;  b' = rho b + g;  theta' = theta - nu (g + rho b')
+__device__ __forceinline__ void nesterov(double dhat, float th, float b, double lr, double rho,
+                                         float& th_out, float& b_out) {
+  const double g = -dhat;
+  const double bn = fma(rho, static_cast<double>(b), g);
+  th_out = static_cast<float>(static_cast<double>(th) - lr * fma(rho, bn, g));
+  b_out = static_cast<float>(bn);
+}
+
 template <int K, bool BF16>
 __global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restrict__ theta,
                                                                 float* __restrict__ mom,
                                                                 MutPtrs<K> reps,
                                                                 const UnitRecord* __restrict__ rec,
-                                                                int64_t nvec, int64_t n, float lr,
-                                                                float rho) {
+                                                                int64_t nvec, int64_t n, double lr,
+                                                                double rho) {
   constexpr int VE = Vec<BF16>::VE;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
   const int64_t v0 = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
@@ -363,7 +365,7 @@ __global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restric
     return;
   }
 
-  float c[K];
+  double c[K];
   const uint4* src[K];
 #pragma unroll
   for (int j = 0; j < K; ++j) {
@@ -377,11 +379,12 @@ __global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restric
   const bool use = rec->use_deltas;
 
   for (int64_t v = v0; v < nvec; v += stride) {
-    float th[VE], b[VE], acc[VE];
+    float th[VE], b[VE];
+    double acc[VE];
     load_f32<VE>(theta, v, th);
     load_f32<VE>(mom, v, b);
 #pragma unroll
-    for (int e = 0; e < VE; ++e) acc[e] = 0.f;
+    for (int e = 0; e < VE; ++e) acc[e] = 0.0;
     if (use) {
       uint4 raw[K];
 #pragma unroll
@@ -389,15 +392,11 @@ __global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restric
 #pragma unroll
       for (int j = 0; j < K; ++j)
 #pragma unroll
-        for (int e = 0; e < VE; ++e) acc[e] = fmaf(c[j], element<BF16>(raw[j], e) - th[e], acc[e]);
+        for (int e = 0; e < VE; ++e) acc[e] = fma(c[j], delta64<BF16>(raw[j], e, th[e]), acc[e]);
     }
     float tn[VE], bn[VE];
 #pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      const float g = -acc[e];              // outer gradient, -Delta_hat
-      bn[e] = fmaf(rho, b[e], g);           // b' = rho b + g
-      tn[e] = th[e] - lr * fmaf(rho, bn[e], g);  // theta' = theta - nu (g + rho b')
-    }
+    for (int e = 0; e < VE; ++e) nesterov(acc[e], th[e], b[e], lr, rho, tn[e], bn[e]);
     store_f32<VE>(theta, v, tn);
     store_f32<VE>(mom, v, bn);
     const uint4 out = pack<BF16>(tn);
@@ -407,15 +406,17 @@ __global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restric
 
   if (do_tail) {
     const float th = theta[tail];
-    float acc = 0.f;
+    double acc = 0.0;
     if (use) {
 #pragma unroll
       for (int j = 0; j < K; ++j)
-        acc = fmaf(c[j], load_scalar<BF16>(reinterpret_cast<const void*>(src[j]), tail) - th, acc);
+        acc = fma(c[j],
+                  static_cast<double>(load_scalar<BF16>(reinterpret_cast<const void*>(src[j]), tail)) -
+                      static_cast<double>(th),
+                  acc);
     }
-    const float g = -acc;
-    const float bn = fmaf(rho, mom[tail], g);
-    const float tn = th - lr * fmaf(rho, bn, g);
+    float tn, bn;
+    nesterov(acc, th, mom[tail], lr, rho, tn, bn);
     theta[tail] = tn;
     mom[tail] = bn;
 #pragma unroll
@@ -448,7 +449,7 @@ hipError_t pass1_launch(int blocks, const float* theta, const void* const* reps,
 
 template <int K, bool BF16>
 hipError_t pass2_launch(int blocks, float* theta, float* mom, void* const* reps,
-                        const UnitRecord* rec, int64_t n, float lr, float rho, hipStream_t stream) {
+                        const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
   MutPtrs<K> rp;
   for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
   const int64_t nvec = n / Vec<BF16>::VE;
@@ -506,7 +507,7 @@ hipError_t launch_decide(int K, const double* partials, int rows, UnitRecord* re
 }
 
 hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom, void* const* reps,
-                        const UnitRecord* rec, int64_t n, float lr, float rho, hipStream_t stream) {
+                        const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
   switch (K) {
 #define EDIT_CASE(KK)                                                                          \
   case KK:                                                                                     \

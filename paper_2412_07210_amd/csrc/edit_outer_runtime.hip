@@ -246,8 +246,8 @@ edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta,
   e = launch_decide(K, u.partials, u.rows, u.rec, prm, s);
   if (e != hipSuccess) return fail_hip(e, "decide launch");
   if (prof && (e = hipEventRecord(u.prof[2], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
-  e = launch_pass2(K, bf16, u.blocks2, theta, momentum, mreps, u.rec, n,
-                   static_cast<float>(h->cfg.outer_lr), static_cast<float>(h->cfg.momentum), s);
+  e = launch_pass2(K, bf16, u.blocks2, theta, momentum, mreps, u.rec, n, h->cfg.outer_lr,
+                   h->cfg.momentum, s);
   if (e != hipSuccess) return fail_hip(e, "pass2 launch");
   if (prof && (e = hipEventRecord(u.prof[3], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
   if ((e = hipEventRecord(u.done, s)) != hipSuccess) return fail_hip(e, "hipEventRecord");

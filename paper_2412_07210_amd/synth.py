@@ -237,8 +237,8 @@ def get(name: str) -> Workload:
     return WORKLOADS[name]
 
 
-def small(name: str, numel: Sequence[int], **overrides) -> Workload:
-    """A workload with the recipe of `name` but custom (small) unit sizes."""
-    base = WORKLOADS[name]
+def small(recipe: str, numel: Sequence[int], **overrides) -> Workload:
+    """A workload with the recipe of `recipe` but custom (small) unit sizes."""
+    base = WORKLOADS[recipe]
     units = tuple(((f"flat{i}", int(n), "matrix"),) for i, n in enumerate(numel))
     return replace(base, units=units, **overrides)
