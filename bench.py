@@ -133,6 +133,8 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU-baseline time budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-probe", action="store_true")
+    ap.add_argument("--no-settle", action="store_true",
+                    help="skip the untimed cache settle between input generation and the step")
     args = ap.parse_args(argv)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -171,7 +173,16 @@ def main(argv=None) -> int:
     events = not args.no_kernel_events
     lib.set_profiling(events)
 
-    step_ms, p1_ms, p2_ms, dec_ms = [], [], [], []
+    # Input generation leaves dirty lines of the freshly written replicas in
+    # L2 and the 256 MB Infinity Cache.  Streaming 1 GiB through the copy
+    # kernel (untimed) writes them back, so the timed step starts with its
+    # inputs resident in HBM and pays for no one else's write-backs.
+    settle_src = settle_dst = None
+    if not args.no_settle:
+        settle_src = torch.zeros(256 << 20, dtype=torch.float32, device=dev)
+        settle_dst = torch.empty_like(settle_src)
+
+    step_ms, p1_ms, p2_ms = [], [], []
     p1_bytes = p2_bytes = step_bytes = nominal_bytes = 0
     p1_launches = p2_launches = 0
     masked_total = rollbacks = 0
@@ -189,6 +200,8 @@ def main(argv=None) -> int:
                 hb = [r.view(torch.int16).cpu().numpy().view(np.uint16) if r.dtype == torch.bfloat16
                       else r.cpu().numpy() for r in reps]
                 samples.append((u, th.cpu().numpy().copy(), b.cpu().numpy().copy(), hb))
+        if settle_src is not None:
+            outer.copy_probe(settle_dst, settle_src)
         torch.cuda.synchronize()
         a = torch.cuda.Event(enable_timing=True)
         z = torch.cuda.Event(enable_timing=True)
@@ -210,15 +223,15 @@ def main(argv=None) -> int:
             masked_total += int(st.anomalous.sum())
             rollbacks += int(st.rolled_back)
             if events:
-                k1, kd, k2 = lib.kernel_times(u)
+                k1, k2 = lib.kernel_times(u)
                 p1_ms.append(k1)
-                dec_ms.append(kd)
                 p2_ms.append(k2)
             p1_launches += 1
             p2_launches += 1
         if (t - args.warmup) % 10 == 0:
             log(f"round {t}: {step_ms[-1]:.3f} ms")
     wall = time.time() - t_start
+    del settle_src, settle_dst
 
     total_ms = sum(step_ms)
     ms_per_step = total_ms / len(step_ms)
@@ -247,6 +260,7 @@ def main(argv=None) -> int:
             "replica_dtype": wl.replica_dtype,
             "master_dtype": "f32",
             "streams": args.streams,
+            "cache_settle_before_step": not args.no_settle,
             "parallelism": "single GPU, K replicas reduced in HBM",
         },
         "ms_p10": round(float(q[0]), 4),
@@ -276,8 +290,7 @@ def main(argv=None) -> int:
             "avg_launch_ms": round(avg_ms, 5),
         }
         result["kernels_ms_avg"] = {
-            "pass1_gram": round(sum(p1_ms) / len(p1_ms), 5),
-            "decide": round(sum(dec_ms) / len(dec_ms), 5),
+            "pass1_gram_decide": round(sum(p1_ms) / len(p1_ms), 5),
             "pass2_update": round(avg_ms, 5),
             "pass1_gbps": round((p1_bytes / p1_launches) / (sum(p1_ms) / len(p1_ms) * 1e-3) / 1e9, 2),
         }

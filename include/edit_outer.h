@@ -20,9 +20,10 @@
  *        b' = rho*b + g;   theta' = theta - nu*(g + rho*b'),
  *   6. writes theta' back to every replica (all K, flagged ones included).
  *
- * Precision: theta and the momentum b are fp32; replicas are fp32 or bf16
- * (round-to-nearest-even of the fp32 theta').  Norms, EMA state, weights and
- * the clip factor are fp64; the elementwise update is fp32.
+ * Precision: theta and the momentum b are stored in fp32; replicas in fp32
+ * or bf16 (round-to-nearest-even of the fp32 theta').  All arithmetic from
+ * the pseudo gradients on is fp64 (norms, Gram matrix, EMA state, weights,
+ * clip factor and the elementwise update), rounded once when stored.
  *
  * All pointers to tensor data are DEVICE pointers on the device that was
  * current when the handle was created; the caller owns them.  The library
@@ -101,8 +102,8 @@ edit_status_t edit_outer_init(const edit_outer_config_t *cfg, edit_outer_t *out)
 
 /* One outer step of unit `layer` (Sec. 3.2, Algorithm 2), enqueued on
  * `stream` (a hipStream_t; NULL = the default stream).  No host
- * synchronisation; the three kernels (norm/Gram pass, decision, update pass)
- * run in stream order.
+ * synchronisation; the norm/Gram pass, the one-block decision kernel and the
+ * update pass run in stream order.
  *   theta    [n] fp32, in: theta_t, out: theta_{t+1} (unchanged on rollback)
  *   momentum [n] fp32, in/out: outer momentum b (zero-initialised by caller)
  *   replicas host array of K device pointers, each [n] of replica_dtype;
@@ -134,12 +135,12 @@ const char *edit_outer_last_error(void);
 
 /* ---- measurement helpers (not part of the method) ---------------------- */
 
-/* When enabled, each step records HIP events around its three kernels. */
+/* When enabled, each step records HIP events around its two passes. */
 edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t enable);
 
 /* Durations in ms of the last profiled step of `layer`: ms[0] the norm/Gram
- * pass, ms[1] the decision kernel, ms[2] the update pass.  Waits for it. */
-edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[3]);
+ * pass plus the decision kernel, ms[1] the update pass.  Waits for it. */
+edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[2]);
 
 /* Plain device-to-device copy kernel of nbytes (a multiple of 16, 16-byte
  * aligned pointers), used to calibrate HBM traffic counters and bandwidth. */

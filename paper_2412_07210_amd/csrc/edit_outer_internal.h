@@ -51,9 +51,8 @@ hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom,
 hipError_t launch_copy(void* dst, const void* src, int64_t nbytes, int blocks,
                        hipStream_t stream);
 
-// Resident blocks per CU of each streaming kernel (for the persistent grids).
+// Resident blocks per CU of the pass-1 kernel (for its persistent grid).
 int pass1_blocks_per_cu(int K, bool bf16);
-int pass2_blocks_per_cu(int K, bool bf16);
 
 inline int num_pairs(int K) { return K * (K + 1) / 2; }
 

@@ -9,9 +9,9 @@
 //          ||sum_j w_j Delta_j||^2 = w^T Gram w, so the clip factor of Eq. 4
 //          is known before the update pass and the step needs two streaming
 //          passes instead of three.
-//   decide one block: fixed-order fp64 reduction of the per-block partials,
-//          the EMA z-test and update (Eq. 1), rollback test, softmax weights
-//          (Eq. 2), Gbar and beta (Eq. 4), per-worker coefficients beta*w_j.
+//   decide one block: fixed-order reduction of the per-block partials and the
+//          decision: EMA z-test and update (Eq. 1), rollback test, softmax
+//          weights (Eq. 2), Gbar and beta (Eq. 4), coefficients beta*w_j.
 //   pass2  streams theta, b and the replicas of the workers with a non-zero
 //          coefficient, forms Delta_hat = sum_j beta w_j Delta_j (Eq. 3, 5),
 //          applies Nesterov momentum and writes theta, b and all K replicas.
@@ -19,19 +19,24 @@
 // Storage is fp32 (theta, b) and fp32/bf16 (replicas); arithmetic is fp64
 // from the exact pseudo gradients on, rounded once when stored.
 //
-// The passes are HBM-bound (about 2-3 flop per byte at K = 8), so there is
-// no MFMA: each lane moves 16-byte vectors (global_load_dwordx4), the grid is
-// persistent (resident blocks only, grid-stride over 16-byte vectors) so the
-// whole chip streams one contiguous window of every buffer at a time, and
-// reductions go wave shuffle -> LDS -> per-block partial in a fixed order, so
-// results are bitwise reproducible without atomics.
-#include <type_traits>
-
+// The passes are HBM-bound (2-3 flop per byte at K = 8), so there is no
+// MFMA.  Lanes move 16-byte vectors (global_load_dwordx4).  Pass 1 runs a
+// persistent grid (resident blocks only, grid-stride), so the chip streams
+// one contiguous window of every buffer at a time; each lane double-buffers its
+// vectors (the loads of trip t+1 are in flight while trip t is computed), so
+// the fp64 work hides under the memory latency even at 2 waves per SIMD.
+// Pass 2, which writes as much as it reads, instead gives each thread one
+// vector and lets the block dispatcher order the traffic (see there).
+// Reductions go
+// wave shuffle -> LDS -> per-block partial -> one block in a fixed order, so
+// results are bitwise reproducible.
 #include "edit_outer_internal.h"
 
 namespace edit {
 namespace {
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float float2_t __attribute__((ext_vector_type(2)));
 
@@ -49,15 +54,30 @@ struct Vec {
   static constexpr int VE = BF16 ? 8 : 4;  // elements per 16-byte replica vector
 };
 
+// 16-byte global accesses; NT marks them non-temporal (streaming) in the cache.
+template <bool NT, typename T>
+__device__ __forceinline__ T ld16(const T* p) {
+  if constexpr (NT)
+    return __builtin_nontemporal_load(p);
+  else
+    return *p;
+}
+template <bool NT, typename T>
+__device__ __forceinline__ void st16(T* p, T v) {
+  if constexpr (NT)
+    __builtin_nontemporal_store(v, p);
+  else
+    *p = v;
+}
+
 // Element e of a 16-byte replica vector, widened to fp32 (exact).
 template <bool BF16>
-__device__ __forceinline__ float element(const uint4& raw, int e) {
-  const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+__device__ __forceinline__ float element(const u32x4& raw, int e) {
   if constexpr (BF16) {
-    const uint32_t word = w[e >> 1];
+    const uint32_t word = raw[e >> 1];
     return __uint_as_float((e & 1) ? (word & 0xffff0000u) : (word << 16));
   } else {
-    return __uint_as_float(w[e]);
+    return __uint_as_float(raw[e]);
   }
 }
 
@@ -86,37 +106,49 @@ __device__ __forceinline__ void store_scalar(void* base, int64_t i, float x) {
   }
 }
 
-// theta[v*VE .. v*VE+VE) as fp32.
-template <int VE>
-__device__ __forceinline__ void load_f32(const float* __restrict__ p, int64_t v, float (&x)[VE]) {
-  const float4* q = reinterpret_cast<const float4*>(p) + v * (VE / 4);
+// fp32 values [v*VE, v*VE+VE) of a theta/momentum buffer.
+template <int VE, bool NT>
+__device__ __forceinline__ void load_f32(const float* p, int64_t v, float (&x)[VE]) {
+  const f32x4* q = reinterpret_cast<const f32x4*>(p) + v * (VE / 4);
 #pragma unroll
   for (int h = 0; h < VE / 4; ++h) {
-    const float4 t = q[h];
-    x[4 * h + 0] = t.x;
-    x[4 * h + 1] = t.y;
-    x[4 * h + 2] = t.z;
-    x[4 * h + 3] = t.w;
+    const f32x4 t = ld16<NT>(q + h);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) x[4 * h + c] = t[c];
   }
 }
 
-template <int VE>
-__device__ __forceinline__ void store_f32(float* __restrict__ p, int64_t v, const float (&x)[VE]) {
-  float4* q = reinterpret_cast<float4*>(p) + v * (VE / 4);
+template <int VE, bool NT>
+__device__ __forceinline__ void store_f32(float* p, int64_t v, const float (&x)[VE]) {
+  f32x4* q = reinterpret_cast<f32x4*>(p) + v * (VE / 4);
 #pragma unroll
-  for (int h = 0; h < VE / 4; ++h) q[h] = make_float4(x[4 * h], x[4 * h + 1], x[4 * h + 2], x[4 * h + 3]);
+  for (int h = 0; h < VE / 4; ++h) {
+    f32x4 t;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) t[c] = x[4 * h + c];
+    st16<NT>(q + h, t);
+  }
 }
 
 // VE fp32 values -> one 16-byte replica vector.
 template <bool BF16>
-__device__ __forceinline__ uint4 pack(const float (&x)[Vec<BF16>::VE]) {
+__device__ __forceinline__ u32x4 pack(const float (&x)[Vec<BF16>::VE]) {
+  u32x4 r;
   if constexpr (BF16) {
-    return make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
-                      pack_bf16x2(x[6], x[7]));
+#pragma unroll
+    for (int c = 0; c < 4; ++c) r[c] = pack_bf16x2(x[2 * c], x[2 * c + 1]);
   } else {
-    return make_uint4(__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
-                      __float_as_uint(x[3]));
+#pragma unroll
+    for (int c = 0; c < 4; ++c) r[c] = __float_as_uint(x[c]);
   }
+  return r;
+}
+
+// Element e of a replica vector minus theta, in fp64: the pseudo gradient of
+// that element, exact for fp32/bf16 inputs whose exponents differ by < 29.
+template <bool BF16>
+__device__ __forceinline__ double delta64(const u32x4& raw, int e, float th) {
+  return static_cast<double>(element<BF16>(raw, e)) - static_cast<double>(th);
 }
 
 // Sum over the 64 lanes of a wave, fixed butterfly order (same in every lane).
@@ -126,107 +158,43 @@ __device__ __forceinline__ double wave_sum(double x) {
   return x;
 }
 
-// ---------------------------------------------------------------- pass 1
-
-// Element e of a 16-byte replica vector minus theta, in fp64: the pseudo
-// gradient of that element, exact for every pair of fp32/bf16 inputs whose
-// exponents differ by less than 29.
-template <bool BF16>
-__device__ __forceinline__ double delta64(const uint4& raw, int e, float th) {
-  return static_cast<double>(element<BF16>(raw, e)) - static_cast<double>(th);
-}
-
-template <int K, bool BF16>
-__global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __restrict__ theta,
-                                                              ConstPtrs<K> reps, int64_t nvec,
-                                                              int64_t n,
-                                                              double* __restrict__ partials) {
-  constexpr int NP = K * (K + 1) / 2;
-  constexpr int VE = Vec<BF16>::VE;
-  // fp64 products and sums: on CDNA3/4 a v_fma_f64 issues at the rate of an
-  // unpacked v_fma_f32, so exactness costs no extra VALU cycles, and the
-  // Gram identity for ||sum_j w_j Delta_j|| stays accurate even when the
-  // workers' pseudo gradients nearly cancel.
-  double acc[NP];
-#pragma unroll
-  for (int p = 0; p < NP; ++p) acc[p] = 0.0;
-
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
-  for (int64_t v = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; v < nvec; v += stride) {
-    float th[VE];
-    load_f32<VE>(theta, v, th);
-    uint4 raw[K];
-#pragma unroll
-    for (int j = 0; j < K; ++j) raw[j] = reinterpret_cast<const uint4*>(reps.p[j])[v];
-#pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      double d[K];
-#pragma unroll
-      for (int j = 0; j < K; ++j) d[j] = delta64<BF16>(raw[j], e, th[e]);
-      int p = 0;
-#pragma unroll
-      for (int j = 0; j < K; ++j)
-#pragma unroll
-        for (int k = j; k < K; ++k, ++p) acc[p] = fma(d[j], d[k], acc[p]);
-    }
-  }
-
-  // Ragged tail (fewer than VE elements past the last full vector): block 0.
-  const int64_t i = nvec * VE + threadIdx.x;
-  if (blockIdx.x == 0 && i < n) {
-    double d[K];
-    const double th = theta[i];
-#pragma unroll
-    for (int j = 0; j < K; ++j) d[j] = static_cast<double>(load_scalar<BF16>(reps.p[j], i)) - th;
-    int p = 0;
-#pragma unroll
-    for (int j = 0; j < K; ++j)
-#pragma unroll
-      for (int k = j; k < K; ++k, ++p) acc[p] = fma(d[j], d[k], acc[p]);
-  }
-
-  // Block reduction: wave butterfly, then the four waves in order.
-  __shared__ double red[kThreads / 64][NP];
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    const double s = wave_sum(acc[p]);
-    if (lane == 0) red[wave][p] = s;
-  }
-  __syncthreads();
-  const int rows = gridDim.x;
-  for (int p = threadIdx.x; p < NP; p += kThreads) {
-    double s = red[0][p];
-#pragma unroll
-    for (int w = 1; w < kThreads / 64; ++w) s += red[w][p];
-    partials[static_cast<int64_t>(p) * rows + blockIdx.x] = s;
-  }
-}
-
-// ---------------------------------------------------------------- decide
-
 __device__ __forceinline__ int pair_index(int K, int j, int k) {  // j <= k
   return j * K - (j * (j - 1)) / 2 + (k - j);
 }
 
+// ------------------------------------------------------------- decision
+
+// Reduce the per-block Gram partials [NP][rows] in a fixed order into
+// gram[NP] (shared memory).  Called by every thread of one block.
 template <int K>
-__global__ __launch_bounds__(kThreads) void decide_kernel(const double* __restrict__ partials,
-                                                          int rows, UnitRecord* __restrict__ rec,
-                                                          DecideParams prm) {
+__device__ void reduce_partials(const double* partials, int rows, double* gram) {
   constexpr int NP = K * (K + 1) / 2;
-  __shared__ double gram[NP];
+  constexpr int kWaves = kThreads / 64;
+  constexpr int PPW = (NP + kWaves - 1) / kWaves;  // pairs per wave
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  for (int p = wave; p < NP; p += kThreads / 64) {
-    double s = 0.0;
-    for (int r = lane; r < rows; r += 64) s += partials[static_cast<int64_t>(p) * rows + r];
-    s = wave_sum(s);
-    if (lane == 0) gram[p] = s;
+  double s[PPW];
+#pragma unroll
+  for (int q = 0; q < PPW; ++q) s[q] = 0.0;
+#pragma unroll 2
+  for (int r = lane; r < rows; r += 64) {
+#pragma unroll
+    for (int q = 0; q < PPW; ++q) {
+      const int p = wave + kWaves * q;
+      if (p < NP) s[q] += __builtin_nontemporal_load(partials + static_cast<int64_t>(p) * rows + r);
+    }
   }
-  __syncthreads();
-  if (threadIdx.x != 0) return;
+#pragma unroll
+  for (int q = 0; q < PPW; ++q) {
+    const int p = wave + kWaves * q;
+    const double t = wave_sum(s[q]);
+    if (lane == 0 && p < NP) gram[p] = t;
+  }
+}
 
+// The decision of one step from the unit's Gram matrix (one thread).
+template <int K>
+__device__ void decide(const double* gram, UnitRecord* rec, const DecideParams& prm) {
   const bool ae = prm.flags & EDIT_AE;
   const bool wa = prm.flags & EDIT_WA;
   const bool gc = prm.flags & EDIT_GC;
@@ -302,18 +270,19 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const double* __restri
   }
 
   int first = -1;
+  double c[K];
 #pragma unroll
   for (int j = 0; j < K; ++j) {
-    const double c = beta * w[j];
+    c[j] = beta * w[j];
     rec->weight[j] = w[j];
-    rec->coef[j] = c;
-    if (c != 0.0 && first < 0) first = j;
+    rec->coef[j] = c[j];
+    if (c[j] != 0.0 && first < 0) first = j;
   }
   // The update pass loads slot j from worker src[j]: itself when it
   // contributes, otherwise a contributing worker (a cache hit, and never the
   // data of a flagged worker, which may hold NaN).
 #pragma unroll
-  for (int j = 0; j < K; ++j) rec->src[j] = (rec->coef[j] != 0.0 || first < 0) ? j : first;
+  for (int j = 0; j < K; ++j) rec->src[j] = (c[j] != 0.0 || first < 0) ? j : first;
   rec->use_deltas = first >= 0 ? 1 : 0;
   rec->rollback = n_ok == 0 ? 1 : 0;
   rec->synced_norm = gbar;
@@ -321,6 +290,128 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const double* __restri
   rec->z_tested = z_test ? 1 : 0;
   rec->stepped = 1;
   rec->round = t + 1;
+}
+
+// ---------------------------------------------------------------- pass 1
+
+// Gram contributions of one 16-byte vector of every replica.
+template <int K, bool BF16>
+__device__ __forceinline__ void gram_vector(double (&acc)[K * (K + 1) / 2], const u32x4 (&raw)[K],
+                                            const float (&th)[Vec<BF16>::VE]) {
+#pragma unroll
+  for (int e = 0; e < Vec<BF16>::VE; ++e) {
+    double d[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) d[j] = delta64<BF16>(raw[j], e, th[e]);
+    int p = 0;
+#pragma unroll
+    for (int j = 0; j < K; ++j)
+#pragma unroll
+      for (int k = j; k < K; ++k, ++p) acc[p] = fma(d[j], d[k], acc[p]);
+  }
+}
+
+// theta and every replica at vector v; zeros past the end (they add nothing).
+template <int K, bool BF16, bool NT>
+__device__ __forceinline__ void load_pass1(const float* theta, const ConstPtrs<K>& reps, int64_t v,
+                                           int64_t nvec, float (&th)[Vec<BF16>::VE], u32x4 (&raw)[K]) {
+  if (v < nvec) {
+    load_f32<Vec<BF16>::VE, NT>(theta, v, th);
+#pragma unroll
+    for (int j = 0; j < K; ++j) raw[j] = ld16<NT>(reinterpret_cast<const u32x4*>(reps.p[j]) + v);
+  } else {
+#pragma unroll
+    for (int e = 0; e < Vec<BF16>::VE; ++e) th[e] = 0.f;
+#pragma unroll
+    for (int j = 0; j < K; ++j) raw[j] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+template <int K, bool BF16, bool NT>
+__global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __restrict__ theta,
+                                                              ConstPtrs<K> reps, int64_t nvec,
+                                                              int64_t n,
+                                                              double* __restrict__ partials) {
+  constexpr int NP = K * (K + 1) / 2;
+  constexpr int VE = Vec<BF16>::VE;
+  // fp64 products and sums: on CDNA3/4 a v_fma_f64 issues at the rate of an
+  // unpacked v_fma_f32, so exactness costs no extra VALU cycles, and the
+  // Gram identity for ||sum_j w_j Delta_j|| stays accurate even when the
+  // workers' pseudo gradients nearly cancel.
+  double acc[NP];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) acc[p] = 0.0;
+
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
+  int64_t v = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+  if constexpr (K <= 8) {
+    // Double-buffered grid-stride loop: buffer A holds trip t, B trip t+1.
+    float thA[VE], thB[VE];
+    u32x4 rA[K], rB[K];
+    load_pass1<K, BF16, NT>(theta, reps, v, nvec, thA, rA);
+    while (v < nvec) {
+      load_pass1<K, BF16, NT>(theta, reps, v + stride, nvec, thB, rB);
+      gram_vector<K, BF16>(acc, rA, thA);
+      v += stride;
+      if (v >= nvec) break;
+      load_pass1<K, BF16, NT>(theta, reps, v + stride, nvec, thA, rA);
+      gram_vector<K, BF16>(acc, rB, thB);
+      v += stride;
+    }
+  } else {
+    // K > 8: the K(K+1)/2 fp64 accumulators leave no registers for a
+    // second buffer.
+    for (; v < nvec; v += stride) {
+      float th[VE];
+      u32x4 raw[K];
+      load_pass1<K, BF16, NT>(theta, reps, v, nvec, th, raw);
+      gram_vector<K, BF16>(acc, raw, th);
+    }
+  }
+
+  // Ragged tail (fewer than VE elements past the last full vector): block 0.
+  const int64_t i = nvec * VE + threadIdx.x;
+  if (blockIdx.x == 0 && i < n) {
+    double d[K];
+    const double th = theta[i];
+#pragma unroll
+    for (int j = 0; j < K; ++j) d[j] = static_cast<double>(load_scalar<BF16>(reps.p[j], i)) - th;
+    int p = 0;
+#pragma unroll
+    for (int j = 0; j < K; ++j)
+#pragma unroll
+      for (int k = j; k < K; ++k, ++p) acc[p] = fma(d[j], d[k], acc[p]);
+  }
+
+  // Block reduction: wave butterfly, then the four waves in order.
+  __shared__ double red[kThreads / 64][NP];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const double s = wave_sum(acc[p]);
+    if (lane == 0) red[wave][p] = s;
+  }
+  __syncthreads();
+  const int rows = gridDim.x;
+  for (int p = threadIdx.x; p < NP; p += kThreads) {
+    double s = red[0][p];
+#pragma unroll
+    for (int w = 1; w < kThreads / 64; ++w) s += red[w][p];
+    partials[static_cast<int64_t>(p) * rows + blockIdx.x] = s;
+  }
+}
+
+// ---------------------------------------------------------------- decide
+
+template <int K>
+__global__ __launch_bounds__(kThreads) void decide_kernel(const double* __restrict__ partials,
+                                                          int rows, UnitRecord* __restrict__ rec,
+                                                          DecideParams prm) {
+  __shared__ double gram[K * (K + 1) / 2];
+  reduce_partials<K>(partials, rows, gram);
+  __syncthreads();
+  if (threadIdx.x == 0) decide<K>(gram, rec, prm);
 }
 
 // ---------------------------------------------------------------- pass 2
@@ -336,7 +427,55 @@ __device__ __forceinline__ void nesterov(double dhat, float th, float b, double 
   b_out = static_cast<float>(bn);
 }
 
-template <int K, bool BF16>
+// theta, b and the contributing replicas at vector v (nothing past the end).
+template <int K, bool BF16, bool NT>
+__device__ __forceinline__ void load_pass2(const float* theta, const float* mom,
+                                           const u32x4* const (&src)[K], bool use, int64_t v,
+                                           int64_t nvec, float (&th)[Vec<BF16>::VE],
+                                           float (&b)[Vec<BF16>::VE], u32x4 (&raw)[K]) {
+  if (v < nvec) {
+    load_f32<Vec<BF16>::VE, NT>(theta, v, th);
+    load_f32<Vec<BF16>::VE, NT>(mom, v, b);
+    if (use) {
+#pragma unroll
+      for (int j = 0; j < K; ++j) raw[j] = ld16<NT>(src[j] + v);
+    }
+  }
+}
+
+// The update of one vector: weighted average, Nesterov, write-back.
+template <int K, bool BF16, bool NT>
+__device__ __forceinline__ void update_vector(float* theta, float* mom, const MutPtrs<K>& reps,
+                                              const double (&c)[K], bool use, int64_t v,
+                                              const float (&th)[Vec<BF16>::VE],
+                                              const float (&b)[Vec<BF16>::VE],
+                                              const u32x4 (&raw)[K], double lr, double rho) {
+  constexpr int VE = Vec<BF16>::VE;
+  double acc[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) acc[e] = 0.0;
+  if (use) {
+#pragma unroll
+    for (int j = 0; j < K; ++j)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) acc[e] = fma(c[j], delta64<BF16>(raw[j], e, th[e]), acc[e]);
+  }
+  float tn[VE], bn[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) nesterov(acc[e], th[e], b[e], lr, rho, tn[e], bn[e]);
+  store_f32<VE, NT>(theta, v, tn);
+  store_f32<VE, NT>(mom, v, bn);
+  const u32x4 out = pack<BF16>(tn);
+#pragma unroll
+  for (int j = 0; j < K; ++j) st16<NT>(reinterpret_cast<u32x4*>(reps.p[j]) + v, out);
+}
+
+// One 16-byte vector of every buffer per thread, one block per 256 vectors,
+// blocks taken from the unit's end: the hardware dispatcher then keeps the
+// in-flight window of each of the 2K+4 streams short and ordered (measured
+// 5.5 TB/s here against 4.9 TB/s for a persistent grid-stride loop), and the
+// first blocks read what pass 1 read last, still in the Infinity Cache.
+template <int K, bool BF16, bool NT>
 __global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restrict__ theta,
                                                                 float* __restrict__ mom,
                                                                 MutPtrs<K> reps,
@@ -344,18 +483,17 @@ __global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restric
                                                                 int64_t nvec, int64_t n, double lr,
                                                                 double rho) {
   constexpr int VE = Vec<BF16>::VE;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
-  const int64_t v0 = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+  const int64_t v = static_cast<int64_t>(gridDim.x - 1 - blockIdx.x) * kThreads + threadIdx.x;
   const int64_t tail = nvec * VE + threadIdx.x;
   const bool do_tail = blockIdx.x == 0 && tail < n;
 
   if (rec->rollback) {  // every worker flagged: replicas <- theta_t, nothing else moves
-    for (int64_t v = v0; v < nvec; v += stride) {
+    if (v < nvec) {
       float th[VE];
-      load_f32<VE>(theta, v, th);
-      const uint4 out = pack<BF16>(th);
+      load_f32<VE, NT>(theta, v, th);
+      const u32x4 out = pack<BF16>(th);
 #pragma unroll
-      for (int j = 0; j < K; ++j) reinterpret_cast<uint4*>(reps.p[j])[v] = out;
+      for (int j = 0; j < K; ++j) st16<NT>(reinterpret_cast<u32x4*>(reps.p[j]) + v, out);
     }
     if (do_tail) {
       const float th = theta[tail];
@@ -366,7 +504,7 @@ __global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restric
   }
 
   double c[K];
-  const uint4* src[K];
+  const u32x4* src[K];
 #pragma unroll
   for (int j = 0; j < K; ++j) {
     c[j] = rec->coef[j];
@@ -374,34 +512,15 @@ __global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restric
     const void* ptr = reps.p[0];
 #pragma unroll
     for (int i = 1; i < K; ++i) ptr = (s == i) ? reps.p[i] : ptr;
-    src[j] = reinterpret_cast<const uint4*>(ptr);
+    src[j] = reinterpret_cast<const u32x4*>(ptr);
   }
   const bool use = rec->use_deltas;
 
-  for (int64_t v = v0; v < nvec; v += stride) {
+  if (v < nvec) {
     float th[VE], b[VE];
-    double acc[VE];
-    load_f32<VE>(theta, v, th);
-    load_f32<VE>(mom, v, b);
-#pragma unroll
-    for (int e = 0; e < VE; ++e) acc[e] = 0.0;
-    if (use) {
-      uint4 raw[K];
-#pragma unroll
-      for (int j = 0; j < K; ++j) raw[j] = src[j][v];
-#pragma unroll
-      for (int j = 0; j < K; ++j)
-#pragma unroll
-        for (int e = 0; e < VE; ++e) acc[e] = fma(c[j], delta64<BF16>(raw[j], e, th[e]), acc[e]);
-    }
-    float tn[VE], bn[VE];
-#pragma unroll
-    for (int e = 0; e < VE; ++e) nesterov(acc[e], th[e], b[e], lr, rho, tn[e], bn[e]);
-    store_f32<VE>(theta, v, tn);
-    store_f32<VE>(mom, v, bn);
-    const uint4 out = pack<BF16>(tn);
-#pragma unroll
-    for (int j = 0; j < K; ++j) reinterpret_cast<uint4*>(reps.p[j])[v] = out;
+    u32x4 raw[K];
+    load_pass2<K, BF16, NT>(theta, mom, src, use, v, nvec, th, b, raw);
+    update_vector<K, BF16, NT>(theta, mom, reps, c, use, v, th, b, raw, lr, rho);
   }
 
   if (do_tail) {
@@ -426,15 +545,34 @@ __global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restric
 
 // ------------------------------------------------------------ copy probe
 
-__global__ __launch_bounds__(kThreads) void copy_kernel(uint4* __restrict__ dst,
-                                                       const uint4* __restrict__ src,
+template <int U, bool NT>
+__global__ __launch_bounds__(kThreads) void copy_kernel(u32x4* __restrict__ dst,
+                                                       const u32x4* __restrict__ src,
                                                        int64_t nvec) {
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
-  for (int64_t v = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; v < nvec; v += stride)
-    dst[v] = src[v];
+  for (int64_t v = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; v < nvec; v += stride * U) {
+    u32x4 x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (u == 0 || v + u * stride < nvec) x[u] = ld16<NT>(src + v + u * stride);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (u == 0 || v + u * stride < nvec) st16<NT>(dst + v + u * stride, x[u]);
+  }
 }
 
+}  // namespace
+
 // ------------------------------------------------------------ launchers
+
+// Cache policy of the streaming kernels: the update pass touches every byte
+// once, and non-temporal accesses measured ~5% faster there.
+constexpr bool kNT1 = false;
+constexpr bool kNT2 = true;
+constexpr int kUnrollCopy = 1;
+constexpr bool kNTCopy = false;
+
+namespace {
 
 template <int K, bool BF16>
 hipError_t pass1_launch(int blocks, const float* theta, const void* const* reps, int64_t n,
@@ -442,8 +580,15 @@ hipError_t pass1_launch(int blocks, const float* theta, const void* const* reps,
   ConstPtrs<K> rp;
   for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
   const int64_t nvec = n / Vec<BF16>::VE;
-  hipLaunchKernelGGL((pass1_gram_kernel<K, BF16>), dim3(blocks), dim3(kThreads), 0, stream, theta,
-                     rp, nvec, n, partials);
+  hipLaunchKernelGGL((pass1_gram_kernel<K, BF16, kNT1>), dim3(blocks), dim3(kThreads), 0, stream,
+                     theta, rp, nvec, n, partials);
+  return hipGetLastError();
+}
+
+template <int K>
+hipError_t decide_launch(const double* partials, int rows, UnitRecord* rec, const DecideParams& prm,
+                         hipStream_t stream) {
+  hipLaunchKernelGGL((decide_kernel<K>), dim3(1), dim3(kThreads), 0, stream, partials, rows, rec, prm);
   return hipGetLastError();
 }
 
@@ -453,15 +598,8 @@ hipError_t pass2_launch(int blocks, float* theta, float* mom, void* const* reps,
   MutPtrs<K> rp;
   for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
   const int64_t nvec = n / Vec<BF16>::VE;
-  hipLaunchKernelGGL((pass2_update_kernel<K, BF16>), dim3(blocks), dim3(kThreads), 0, stream, theta,
-                     mom, rp, rec, nvec, n, lr, rho);
-  return hipGetLastError();
-}
-
-template <int K>
-hipError_t decide_launch(const double* partials, int rows, UnitRecord* rec, const DecideParams& prm,
-                         hipStream_t stream) {
-  hipLaunchKernelGGL((decide_kernel<K>), dim3(1), dim3(kThreads), 0, stream, partials, rows, rec, prm);
+  hipLaunchKernelGGL((pass2_update_kernel<K, BF16, kNT2>), dim3(blocks), dim3(kThreads), 0, stream,
+                     theta, mom, rp, rec, nvec, n, lr, rho);
   return hipGetLastError();
 }
 
@@ -482,9 +620,9 @@ int occupancy(Kern kernel) {
 hipError_t launch_pass1(int K, bool bf16, int blocks, const float* theta, const void* const* reps,
                         int64_t n, double* partials, hipStream_t stream) {
   switch (K) {
-#define EDIT_CASE(KK)                                                                        \
-  case KK:                                                                                   \
-    return bf16 ? pass1_launch<KK, true>(blocks, theta, reps, n, partials, stream)           \
+#define EDIT_CASE(KK)                                                                    \
+  case KK:                                                                               \
+    return bf16 ? pass1_launch<KK, true>(blocks, theta, reps, n, partials, stream)       \
                 : pass1_launch<KK, false>(blocks, theta, reps, n, partials, stream);
     EDIT_FOR_EACH_K(EDIT_CASE)
 #undef EDIT_CASE
@@ -521,28 +659,17 @@ hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom, 
 }
 
 hipError_t launch_copy(void* dst, const void* src, int64_t nbytes, int blocks, hipStream_t stream) {
-  hipLaunchKernelGGL(copy_kernel, dim3(blocks), dim3(kThreads), 0, stream,
-                     reinterpret_cast<uint4*>(dst), reinterpret_cast<const uint4*>(src), nbytes / 16);
+  hipLaunchKernelGGL((copy_kernel<kUnrollCopy, kNTCopy>), dim3(blocks), dim3(kThreads), 0, stream,
+                     reinterpret_cast<u32x4*>(dst), reinterpret_cast<const u32x4*>(src), nbytes / 16);
   return hipGetLastError();
 }
 
 int pass1_blocks_per_cu(int K, bool bf16) {
   switch (K) {
-#define EDIT_CASE(KK) \
-  case KK:            \
-    return bf16 ? occupancy(pass1_gram_kernel<KK, true>) : occupancy(pass1_gram_kernel<KK, false>);
-    EDIT_FOR_EACH_K(EDIT_CASE)
-#undef EDIT_CASE
-    default:
-      return 1;
-  }
-}
-
-int pass2_blocks_per_cu(int K, bool bf16) {
-  switch (K) {
-#define EDIT_CASE(KK) \
-  case KK:            \
-    return bf16 ? occupancy(pass2_update_kernel<KK, true>) : occupancy(pass2_update_kernel<KK, false>);
+#define EDIT_CASE(KK)                                                          \
+  case KK:                                                                     \
+    return bf16 ? occupancy(pass1_gram_kernel<KK, true, kNT1>)                 \
+                : occupancy(pass1_gram_kernel<KK, false, kNT1>);
     EDIT_FOR_EACH_K(EDIT_CASE)
 #undef EDIT_CASE
     default:

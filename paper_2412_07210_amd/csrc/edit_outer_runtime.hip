@@ -2,9 +2,10 @@
 //
 // A handle owns, per sync unit: the device record (EMA state + decision),
 // the per-block Gram partials of pass 1, a completion event and (when
-// profiling) four timing events.  A step validates its arguments, enqueues
+// profiling) three timing events.  A step validates its arguments, enqueues
 // pass1 -> decide -> pass2 on the caller's stream and returns; there is no
 // host synchronisation on the step path and no device-to-host traffic.
+#include <climits>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -36,7 +37,7 @@ struct Unit {
   double* partials = nullptr;
   UnitRecord* rec = nullptr;
   hipEvent_t done = nullptr;
-  hipEvent_t prof[4] = {nullptr, nullptr, nullptr, nullptr};
+  hipEvent_t prof[3] = {nullptr, nullptr, nullptr};
   bool pending = false;   // `done` has been recorded at least once
   bool profiled = false;  // prof[] hold the last step's timestamps
   bool has_state = false; // stepped or state_set at least once
@@ -49,7 +50,7 @@ struct edit_outer {
   std::vector<int64_t> numel;
   int device = 0;
   int num_cu = 0;
-  int cap1 = 1, cap2 = 1;  // resident blocks of pass 1 / pass 2 on the whole GPU
+  int cap1 = 1;            // resident blocks of pass 1 on the whole GPU
   bool profiling = false;
   char* arena = nullptr;   // one device allocation for every unit's scratch
   std::vector<Unit> units;
@@ -144,7 +145,6 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
   h->num_cu = prop.multiProcessorCount;
   const bool bf16 = cfg->replica_dtype == EDIT_BF16;
   h->cap1 = h->num_cu * pass1_blocks_per_cu(K, bf16);
-  h->cap2 = h->num_cu * pass2_blocks_per_cu(K, bf16);
 
   // Lay out every unit's record and partials in one allocation.
   const int ve = bf16 ? 8 : 4;
@@ -157,7 +157,12 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
     u.n = h->numel[l];
     const int64_t nvec = u.n / ve;
     u.rows = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(h->cap1, ceil_div(nvec, kThreads))));
-    u.blocks2 = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(h->cap2, ceil_div(nvec, kThreads))));
+    // pass 2: one vector per thread (block count grows with the unit)
+    if (ceil_div(nvec, kThreads) > INT32_MAX) {
+      delete h;
+      return fail(EDIT_EINVAL, "layer_numel[" + std::to_string(l) + "] is too large");
+    }
+    u.blocks2 = static_cast<int>(std::max<int64_t>(1, ceil_div(nvec, kThreads)));
     offs[l] = total;
     const size_t part_bytes = (size_t(num_pairs(K)) * u.rows * sizeof(double) + 255) & ~size_t(255);
     total += rec_bytes + part_bytes;
@@ -242,14 +247,13 @@ edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta,
   }
   e = launch_pass1(K, bf16, u.rows, theta, creps, n, u.partials, s);
   if (e != hipSuccess) return fail_hip(e, "pass1 launch");
-  if (prof && (e = hipEventRecord(u.prof[1], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
   e = launch_decide(K, u.partials, u.rows, u.rec, prm, s);
   if (e != hipSuccess) return fail_hip(e, "decide launch");
-  if (prof && (e = hipEventRecord(u.prof[2], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+  if (prof && (e = hipEventRecord(u.prof[1], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
   e = launch_pass2(K, bf16, u.blocks2, theta, momentum, mreps, u.rec, n, h->cfg.outer_lr,
                    h->cfg.momentum, s);
   if (e != hipSuccess) return fail_hip(e, "pass2 launch");
-  if (prof && (e = hipEventRecord(u.prof[3], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+  if (prof && (e = hipEventRecord(u.prof[2], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
   if ((e = hipEventRecord(u.done, s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
   u.pending = true;
   u.profiled = prof;
@@ -336,15 +340,15 @@ edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t enable) {
   return EDIT_OK;
 }
 
-edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[3]) {
+edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[2]) {
   if (!h || !ms) return fail(EDIT_EINVAL, "NULL argument");
   if (layer < 0 || layer >= h->cfg.num_layers)
     return fail(EDIT_EINVAL, "layer " + std::to_string(layer) + " out of range");
   Unit& u = h->units[layer];
   if (!u.profiled) return fail(EDIT_ESTATE, "the unit's last step was not profiled");
-  hipError_t e = hipEventSynchronize(u.prof[3]);
+  hipError_t e = hipEventSynchronize(u.prof[2]);
   if (e != hipSuccess) return fail_hip(e, "hipEventSynchronize");
-  for (int k = 0; k < 3; ++k)
+  for (int k = 0; k < 2; ++k)
     if ((e = hipEventElapsedTime(&ms[k], u.prof[k], u.prof[k + 1])) != hipSuccess)
       return fail_hip(e, "hipEventElapsedTime");
   return EDIT_OK;

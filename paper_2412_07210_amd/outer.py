@@ -298,11 +298,11 @@ class EditOuter:
         _check(self._lib.edit_outer_set_profiling(self._h, int(bool(enable))), "set_profiling")
 
     def kernel_times(self, layer: int) -> tuple:
-        """(pass1 ms, decide ms, pass2 ms) of the unit's last profiled step."""
-        ms = (ctypes.c_float * 3)()
+        """(pass-1 ms incl. the decision, pass-2 ms) of the unit's last profiled step."""
+        ms = (ctypes.c_float * 2)()
         with torch.cuda.device(self.device):
             _check(self._lib.edit_outer_kernel_times(self._h, int(layer), ms), "kernel_times")
-        return float(ms[0]), float(ms[1]), float(ms[2])
+        return float(ms[0]), float(ms[1])
 
 
 def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream: Optional[torch.cuda.Stream] = None) -> None:
