@@ -125,7 +125,7 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=90)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="c3", help="workload: c1..c5")
-    ap.add_argument("--streams", type=int, default=2, help="HIP streams for the unit pipeline")
+    ap.add_argument("--streams", type=int, default=1, help="HIP streams for the unit pipeline")
     ap.add_argument("--units", type=int, default=0, help="use only the first N units (0 = all)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-kernel-events", action="store_true",

@@ -9,9 +9,10 @@
 //          ||sum_j w_j Delta_j||^2 = w^T Gram w, so the clip factor of Eq. 4
 //          is known before the update pass and the step needs two streaming
 //          passes instead of three.
-//   decide one block: fixed-order reduction of the per-block partials and the
-//          decision: EMA z-test and update (Eq. 1), rollback test, softmax
-//          weights (Eq. 2), Gbar and beta (Eq. 4), coefficients beta*w_j.
+//   decide one block: fixed-order reduction of the per-block partials, then
+//          one wave (worker j in lane j) takes the decision: EMA z-test and
+//          update (Eq. 1), rollback test, softmax weights (Eq. 2), Gbar and
+//          beta (Eq. 4), coefficients beta*w_j.
 //   pass2  streams theta, b and the replicas of the workers with a non-zero
 //          coefficient, forms Delta_hat = sum_j beta w_j Delta_j (Eq. 3, 5),
 //          applies Nesterov momentum and writes theta, b and all K replicas.
@@ -164,19 +165,21 @@ __device__ __forceinline__ int pair_index(int K, int j, int k) {  // j <= k
 
 // ------------------------------------------------------------- decision
 
+constexpr int kDecideThreads = 1024;  // one block; wide so the partial loads overlap
+
 // Reduce the per-block Gram partials [NP][rows] in a fixed order into
-// gram[NP] (shared memory).  Called by every thread of one block.
+// gram[NP] (shared memory).  Called by every thread of the decision block.
 template <int K>
 __device__ void reduce_partials(const double* partials, int rows, double* gram) {
   constexpr int NP = K * (K + 1) / 2;
-  constexpr int kWaves = kThreads / 64;
+  constexpr int kWaves = kDecideThreads / 64;
   constexpr int PPW = (NP + kWaves - 1) / kWaves;  // pairs per wave
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   double s[PPW];
 #pragma unroll
   for (int q = 0; q < PPW; ++q) s[q] = 0.0;
-#pragma unroll 2
+#pragma unroll 4
   for (int r = lane; r < rows; r += 64) {
 #pragma unroll
     for (int q = 0; q < PPW; ++q) {
@@ -192,104 +195,92 @@ __device__ void reduce_partials(const double* partials, int rows, double* gram) 
   }
 }
 
-// The decision of one step from the unit's Gram matrix (one thread).
+// The decision of one step from the unit's Gram matrix, taken by one wave:
+// worker j's norm, z-test, EMA update and softmax term live in lane j; the
+// cross-lane steps (min, sums, first contributing worker) are fixed-order
+// butterflies and ballots, so the result is reproducible bit for bit.
 template <int K>
 __device__ void decide(const double* gram, UnitRecord* rec, const DecideParams& prm) {
+  const int lane = threadIdx.x & 63;
   const bool ae = prm.flags & EDIT_AE;
   const bool wa = prm.flags & EDIT_WA;
   const bool gc = prm.flags & EDIT_GC;
   const int64_t t = rec->round;
   const bool z_test = ae && t >= prm.warmup;
+  const bool mine = lane < K;
 
   // Norms and anomaly elimination (Sec. 3.2): the z-test z = (G - mu)/sigma > delta
-  // is taken as G - mu > delta*sigma against the state before this round;
-  // a non-finite norm is always flagged.
-  double G[K];
-  bool bad[K];
-  int n_ok = 0;
-#pragma unroll
-  for (int j = 0; j < K; ++j) {
-    G[j] = sqrt(gram[pair_index(K, j, j)]);
-    bool flag = !isfinite(G[j]);
-    if (z_test && !flag) flag = (G[j] - rec->mu[j]) > prm.delta * rec->sigma[j];
-    bad[j] = flag;
-    n_ok += flag ? 0 : 1;
-    rec->norm[j] = G[j];
-    rec->anomalous[j] = flag ? 1 : 0;
-  }
-  // Eq. 1 for the workers that were not flagged.
-  if (ae) {
-#pragma unroll
-    for (int j = 0; j < K; ++j) {
-      if (bad[j]) continue;
-      const double mu = prm.alpha * G[j] + (1.0 - prm.alpha) * rec->mu[j];
-      const double dev = G[j] - mu;
-      const double sg = rec->sigma[j];
-      rec->sigma[j] = sqrt((1.0 - prm.alpha) * sg * sg + prm.alpha * dev * dev);
-      rec->mu[j] = mu;
+  // is taken as G - mu > delta*sigma against the state before this round; a
+  // non-finite norm is always flagged.  Eq. 1 then updates the unflagged.
+  double G = 0.0;
+  bool bad = true;
+  if (mine) {
+    G = sqrt(gram[pair_index(K, lane, lane)]);
+    bad = !isfinite(G);
+    const double mu0 = rec->mu[lane];
+    const double sg0 = rec->sigma[lane];
+    if (z_test && !bad) bad = (G - mu0) > prm.delta * sg0;
+    rec->norm[lane] = G;
+    rec->anomalous[lane] = bad ? 1 : 0;
+    if (ae && !bad) {
+      const double mu = prm.alpha * G + (1.0 - prm.alpha) * mu0;
+      const double dev = G - mu;
+      rec->sigma[lane] = sqrt((1.0 - prm.alpha) * sg0 * sg0 + prm.alpha * dev * dev);
+      rec->mu[lane] = mu;
     }
   }
+  const bool ok = mine && !bad;
+  const int n_ok = __popcll(__ballot(ok));
 
-  double w[K];
-  double gbar = 0.0, beta = 0.0;
-  if (n_ok == 0) {
-#pragma unroll
-    for (int j = 0; j < K; ++j) w[j] = 0.0;
-  } else {
+  double w = 0.0, gbar = 0.0, beta = 0.0;
+  if (n_ok > 0) {
     if (wa) {  // Eq. 2 as a softmax of -G over the unflagged workers, shifted by min G
-      double g0 = INFINITY;
+      double g0 = ok ? G : INFINITY;
 #pragma unroll
-      for (int j = 0; j < K; ++j)
-        if (!bad[j] && G[j] < g0) g0 = G[j];
-      double gamma = 0.0;
-#pragma unroll
-      for (int j = 0; j < K; ++j) {
-        w[j] = bad[j] ? 0.0 : exp(-(G[j] - g0));
-        gamma += w[j];
-      }
-#pragma unroll
-      for (int j = 0; j < K; ++j) w[j] /= gamma;
+      for (int m = 32; m >= 1; m >>= 1) g0 = fmin(g0, __shfl_xor(g0, m, 64));
+      const double e = ok ? exp(-(G - g0)) : 0.0;
+      w = e / wave_sum(e);
     } else {
-#pragma unroll
-      for (int j = 0; j < K; ++j) w[j] = bad[j] ? 0.0 : 1.0 / n_ok;
+      w = ok ? 1.0 / n_ok : 0.0;
     }
-    // ||sum_j w_j Delta_j||^2 = sum_jk w_j w_k Gram_jk (Eq. 3-4).
+    // ||sum_j w_j Delta_j||^2 = sum_jk w_j w_k Gram_jk (Eq. 3-4); every lane
+    // takes part in every shuffle (uniform trip count).
     double q = 0.0;
 #pragma unroll
-    for (int j = 0; j < K; ++j) {
-      if (bad[j]) continue;
-#pragma unroll
-      for (int k = 0; k < K; ++k) {
-        if (bad[k]) continue;
-        const double g = j <= k ? gram[pair_index(K, j, k)] : gram[pair_index(K, k, j)];
-        q += w[j] * w[k] * g;
-      }
+    for (int it = 0; it < (K * K + 63) / 64; ++it) {
+      const int pk = lane + 64 * it;
+      const int pkc = pk < K * K ? pk : 0;
+      const int j = pkc / K, k = pkc % K;
+      const double wj = __shfl(w, j, 64);
+      const double wk = __shfl(w, k, 64);
+      const double g = j <= k ? gram[pair_index(K, j, k)] : gram[pair_index(K, k, j)];
+      // flagged workers have w = 0 and may have non-finite Gram entries
+      if (pk < K * K && wj != 0.0 && wk != 0.0) q += wj * wk * g;
     }
-    gbar = sqrt(fmax(q, 0.0));
+    gbar = sqrt(fmax(wave_sum(q), 0.0));
     beta = gc ? fmin(prm.phi / (gbar + prm.eps), 1.0) : 1.0;
   }
 
-  int first = -1;
-  double c[K];
-#pragma unroll
-  for (int j = 0; j < K; ++j) {
-    c[j] = beta * w[j];
-    rec->weight[j] = w[j];
-    rec->coef[j] = c[j];
-    if (c[j] != 0.0 && first < 0) first = j;
-  }
   // The update pass loads slot j from worker src[j]: itself when it
   // contributes, otherwise a contributing worker (a cache hit, and never the
   // data of a flagged worker, which may hold NaN).
-#pragma unroll
-  for (int j = 0; j < K; ++j) rec->src[j] = (c[j] != 0.0 || first < 0) ? j : first;
-  rec->use_deltas = first >= 0 ? 1 : 0;
-  rec->rollback = n_ok == 0 ? 1 : 0;
-  rec->synced_norm = gbar;
-  rec->clip_coef = beta;
-  rec->z_tested = z_test ? 1 : 0;
-  rec->stepped = 1;
-  rec->round = t + 1;
+  const double c = beta * w;
+  const unsigned long long nz = __ballot(mine && c != 0.0);
+  const int first = nz ? __ffsll(static_cast<long long>(nz)) - 1 : -1;
+  if (mine) {
+    rec->weight[lane] = w;
+    rec->coef[lane] = c;
+    rec->src[lane] = (c != 0.0 || first < 0) ? lane : first;
+  }
+  if (lane == 0) {
+    rec->use_deltas = first >= 0 ? 1 : 0;
+    rec->rollback = n_ok == 0 ? 1 : 0;
+    rec->synced_norm = gbar;
+    rec->clip_coef = beta;
+    rec->z_tested = z_test ? 1 : 0;
+    rec->stepped = 1;
+    rec->round = t + 1;
+  }
 }
 
 // ---------------------------------------------------------------- pass 1
@@ -405,13 +396,13 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
 // ---------------------------------------------------------------- decide
 
 template <int K>
-__global__ __launch_bounds__(kThreads) void decide_kernel(const double* __restrict__ partials,
-                                                          int rows, UnitRecord* __restrict__ rec,
-                                                          DecideParams prm) {
+__global__ __launch_bounds__(kDecideThreads) void decide_kernel(const double* __restrict__ partials,
+                                                                int rows, UnitRecord* __restrict__ rec,
+                                                                DecideParams prm) {
   __shared__ double gram[K * (K + 1) / 2];
   reduce_partials<K>(partials, rows, gram);
   __syncthreads();
-  if (threadIdx.x == 0) decide<K>(gram, rec, prm);
+  if (threadIdx.x < 64) decide<K>(gram, rec, prm);
 }
 
 // ---------------------------------------------------------------- pass 2
@@ -565,9 +556,9 @@ __global__ __launch_bounds__(kThreads) void copy_kernel(u32x4* __restrict__ dst,
 
 // ------------------------------------------------------------ launchers
 
-// Cache policy of the streaming kernels: the update pass touches every byte
-// once, and non-temporal accesses measured ~5% faster there.
-constexpr bool kNT1 = false;
+// Cache policy of the streaming kernels: both passes touch every byte once;
+// non-temporal accesses measured ~15% faster for pass 1 and ~5% for pass 2.
+constexpr bool kNT1 = true;
 constexpr bool kNT2 = true;
 constexpr int kUnrollCopy = 1;
 constexpr bool kNTCopy = false;
@@ -588,7 +579,8 @@ hipError_t pass1_launch(int blocks, const float* theta, const void* const* reps,
 template <int K>
 hipError_t decide_launch(const double* partials, int rows, UnitRecord* rec, const DecideParams& prm,
                          hipStream_t stream) {
-  hipLaunchKernelGGL((decide_kernel<K>), dim3(1), dim3(kThreads), 0, stream, partials, rows, rec, prm);
+  hipLaunchKernelGGL((decide_kernel<K>), dim3(1), dim3(kDecideThreads), 0, stream, partials, rows, rec,
+                     prm);
   return hipGetLastError();
 }
 
