@@ -119,6 +119,126 @@ def cpu_baseline(samples, wl, seconds_hint: float):
     }
 
 
+# ----------------------------------------------------------------------------
+# Summaries of rocprofv3 output (CPU only): --summarize-profiles
+# ----------------------------------------------------------------------------
+
+PROFILE_CMDS = {
+    "trace": "rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace -o c3 -- "
+             "python bench.py --steps 20 --warmup 10 --no-cpu-baseline",
+    "fetch": "rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/prof_fetch -o c3 -- "
+             "python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0",
+    "write": "rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/prof_write -o c3 -- "
+             "python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0",
+}
+
+
+def _kernel_kind(name: str) -> str:
+    for kind in ("pass1_gram_kernel", "decide_kernel", "pass2_update_kernel", "copy_kernel"):
+        if kind in name:
+            return kind
+    return ""
+
+
+def summarize_profiles(out_dir: str, bench_json: str) -> None:
+    """Turn rocprofv3 CSVs of the 1B K=8 workload into profiles/*.md and the
+    counters file bench.py reads for the roofline's `traffic`."""
+    import csv
+    from paper_2412_07210_amd import synth
+
+    wl = synth.get("c3")
+    n, K, R = wl.layer_numel[0], wl.num_workers, wl.replica_bytes
+    algo = {"pass1_gram_kernel": n * (4 + K * R),
+            "pass2_update_kernel": n * (8 + K * R + 8 + K * R)}
+    algo_rw = {"pass1_gram_kernel": (n * (4 + K * R), 0),
+               "pass2_update_kernel": (n * (8 + K * R), n * (8 + K * R))}
+    prof_dir = os.path.join(ROOT, "profiles")
+    os.makedirs(prof_dir, exist_ok=True)
+    with open(bench_json) as f:
+        bench = json.load(f)
+
+    # kernel trace statistics
+    stats = {}
+    with open(os.path.join(out_dir, "prof_trace", "c3_kernel_stats.csv")) as f:
+        for row in csv.DictReader(f):
+            kind = _kernel_kind(row["Name"])
+            if kind:
+                stats[kind] = {k: float(row[k]) for k in ("Calls", "AverageNs", "MinNs", "MaxNs")}
+    lines = ["# Kernel durations: 1B K=8 outer step (24 units x 51,384,320, bf16 replicas)", "",
+             "Command (from the repository root; `<out>` = gpurun_out):", "",
+             "    " + PROFILE_CMDS["trace"], "",
+             "| kernel | calls | avg us | min us | max us | algorithmic bytes | GB/s at avg |",
+             "|---|---|---|---|---|---|---|"]
+    for kind in ("pass1_gram_kernel", "decide_kernel", "pass2_update_kernel"):
+        st = stats.get(kind)
+        if not st:
+            continue
+        b = algo.get(kind)
+        gbps = f"{b / (st['AverageNs'] * 1e-9) / 1e9:.1f}" if b else "-"
+        lines.append(f"| {kind} | {int(st['Calls'])} | {st['AverageNs'] / 1e3:.1f} | "
+                     f"{st['MinNs'] / 1e3:.1f} | {st['MaxNs'] / 1e3:.1f} | {b if b else '-'} | {gbps} |")
+    rl = bench.get("roofline") or {}
+    if "pass2_update_kernel" in stats and rl:
+        ours = rl["avg_launch_ms"] * 1e3
+        prof = stats["pass2_update_kernel"]["AverageNs"] / 1e3
+        lines += ["", f"bench.py's own HIP-event average for pass2_update_kernel (sampled units, same "
+                  f"workload, default run): {ours:.1f} us; rocprofv3: {prof:.1f} us "
+                  f"({100 * (ours - prof) / prof:+.1f}%)."]
+    with open(os.path.join(prof_dir, "c3_kernel_trace_stats.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+    # HBM counters, calibrated on the 2 GiB copy probe of the same run
+    def counters(tag):
+        per = {}
+        with open(os.path.join(out_dir, f"prof_{tag}", "c3_counter_collection.csv")) as f:
+            for row in csv.DictReader(f):
+                kind = _kernel_kind(row["Kernel_Name"])
+                if kind:
+                    per.setdefault((kind, int(row["Grid_Size"])), []).append(float(row["Counter_Value"]))
+        return per
+
+    fetch, write = counters("fetch"), counters("write")
+    copy_bytes = 2 << 30
+    copy_fetch = max(v for (k, g), vals in fetch.items() if k == "copy_kernel" for v in vals)
+    copy_write = max(v for (k, g), vals in write.items() if k == "copy_kernel" for v in vals)
+    fetch_scale = copy_bytes / (copy_fetch * 1024)
+    write_scale = copy_bytes / (copy_write * 1024)
+    out = {"workload": "c3", "kernel_source_sha256_16": kernel_source_hash(),
+           "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4),
+           "commands": [PROFILE_CMDS["fetch"], PROFILE_CMDS["write"]]}
+    lines = ["# HBM traffic counters: 1B K=8 outer step", "",
+             "Commands (from the repository root; `<out>` = gpurun_out):", "",
+             "    " + PROFILE_CMDS["fetch"], "    " + PROFILE_CMDS["write"], "",
+             f"Calibration on the plain 2 GiB copy kernel in the same runs: FETCH_SIZE reads "
+             f"{copy_fetch:.0f} KiB and WRITE_SIZE {copy_write:.0f} KiB for 2,097,152 KiB moved each "
+             f"way, so FETCH_SIZE is scaled by {fetch_scale:.4f} and WRITE_SIZE by {write_scale:.4f}.", "",
+             "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled bytes/launch | "
+             "algorithmic bytes | ratio |", "|---|---|---|---|---|---|---|"]
+    for kind in ("pass1_gram_kernel", "decide_kernel", "pass2_update_kernel"):
+        fv = [v for (k, g), vals in fetch.items() if k == kind for v in vals]
+        wv = [v for (k, g), vals in write.items() if k == kind for v in vals]
+        if not fv or not wv:
+            continue
+        f_kib, w_kib = sum(fv) / len(fv), sum(wv) / len(wv)
+        traffic = f_kib * 1024 * fetch_scale + w_kib * 1024 * write_scale
+        b = algo.get(kind)
+        ratio = f"{traffic / b:.4f}" if b else "-"
+        lines.append(f"| {kind} | {len(fv)} | {f_kib:.1f} | {w_kib:.1f} | {traffic:.4e} | "
+                     f"{b if b else '-'} | {ratio} |")
+        short = kind.split("_")[0]
+        out[f"{short}_bytes_per_launch"] = round(traffic)
+        out[f"{short}_fetch_kib"] = round(f_kib, 1)
+        out[f"{short}_write_kib"] = round(w_kib, 1)
+        if kind in algo_rw:
+            out[f"{short}_algorithmic_bytes"] = algo[kind]
+    with open(os.path.join(prof_dir, "c3_hbm_counters.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    with open(COUNTERS_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out))
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[1])
     ap.add_argument("--gpus", type=int, default=1)
@@ -128,14 +248,19 @@ def main(argv=None) -> int:
     ap.add_argument("--streams", type=int, default=1, help="HIP streams for the unit pipeline")
     ap.add_argument("--units", type=int, default=0, help="use only the first N units (0 = all)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--no-kernel-events", action="store_true",
-                    help="do not record per-kernel HIP events (roofline then null)")
+    ap.add_argument("--profile-every", type=int, default=6,
+                    help="record per-kernel HIP events on every k-th unit (0: none, roofline then null)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU-baseline time budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-probe", action="store_true")
     ap.add_argument("--no-settle", action="store_true",
                     help="skip the untimed cache settle between input generation and the step")
+    ap.add_argument("--summarize-profiles", nargs=2, metavar=("OUT_DIR", "BENCH_JSON"),
+                    help="write profiles/ summaries from rocprofv3 CSVs under OUT_DIR (no GPU)")
     args = ap.parse_args(argv)
+    if args.summarize_profiles:
+        summarize_profiles(*args.summarize_profiles)
+        return 0
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -170,8 +295,8 @@ def main(argv=None) -> int:
         units.append((th, torch.zeros_like(th), reps))
     torch.cuda.synchronize()
     streams = [torch.cuda.Stream(device=dev) for _ in range(args.streams)] if args.streams > 1 else None
-    events = not args.no_kernel_events
-    lib.set_profiling(events)
+    events = args.profile_every > 0
+    lib.set_profiling(args.profile_every)
 
     # Input generation leaves dirty lines of the freshly written replicas in
     # L2 and the 256 MB Infinity Cache.  Streaming 1 GiB through the copy
@@ -184,6 +309,7 @@ def main(argv=None) -> int:
 
     step_ms, p1_ms, p2_ms = [], [], []
     p1_bytes = p2_bytes = step_bytes = nominal_bytes = 0
+    p1_sample_bytes = p2_sample_bytes = 0
     p1_launches = p2_launches = 0
     masked_total = rollbacks = 0
     samples = []
@@ -222,10 +348,12 @@ def main(argv=None) -> int:
             nominal_bytes += th.numel() * (3 * K * R + 20)
             masked_total += int(st.anomalous.sum())
             rollbacks += int(st.rolled_back)
-            if events:
+            if events and u % args.profile_every == 0:
                 k1, k2 = lib.kernel_times(u)
                 p1_ms.append(k1)
                 p2_ms.append(k2)
+                p1_sample_bytes += b1
+                p2_sample_bytes += b2
             p1_launches += 1
             p2_launches += 1
         if (t - args.warmup) % 10 == 0:
@@ -274,7 +402,8 @@ def main(argv=None) -> int:
         "wall_s": round(wall, 1),
     }
     if events and p2_ms:
-        per_launch = p2_bytes / p2_launches
+        # average over the sampled launches (units 0, k, 2k, ... of every timed step)
+        per_launch = p2_sample_bytes / len(p2_ms)
         avg_ms = sum(p2_ms) / len(p2_ms)
         achieved = per_launch / (avg_ms * 1e-3) / 1e9
         traffic = measured_traffic(per_launch)
@@ -288,11 +417,12 @@ def main(argv=None) -> int:
             "traffic": traffic,
             "bytes_per_launch": int(per_launch),
             "avg_launch_ms": round(avg_ms, 5),
+            "sampled_launches": len(p2_ms),
         }
         result["kernels_ms_avg"] = {
             "pass1_gram_decide": round(sum(p1_ms) / len(p1_ms), 5),
             "pass2_update": round(avg_ms, 5),
-            "pass1_gbps": round((p1_bytes / p1_launches) / (sum(p1_ms) / len(p1_ms) * 1e-3) / 1e9, 2),
+            "pass1_gbps": round((p1_sample_bytes / len(p1_ms)) / (sum(p1_ms) / len(p1_ms) * 1e-3) / 1e9, 2),
         }
     else:
         result["roofline"] = None

@@ -135,8 +135,11 @@ const char *edit_outer_last_error(void);
 
 /* ---- measurement helpers (not part of the method) ---------------------- */
 
-/* When enabled, each step records HIP events around its two passes. */
-edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t enable);
+/* every > 0: steps of units whose index is a multiple of `every` record HIP
+ * events around their two passes (each event costs a few microseconds of
+ * stream time, so a benchmark samples a subset of units); 0 turns it off.
+ * EDIT_EINVAL for every < 0. */
+edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t every);
 
 /* Durations in ms of the last profiled step of `layer`: ms[0] the norm/Gram
  * pass plus the decision kernel, ms[1] the update pass.  Waits for it. */

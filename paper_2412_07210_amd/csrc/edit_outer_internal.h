@@ -9,7 +9,8 @@
 
 namespace edit {
 
-constexpr int kThreads = 256;        // threads per block of the streaming passes
+constexpr int kThreads = 256;        // threads per block of the Gram pass
+constexpr int kPass2Threads = 128;   // threads per block of the update pass
 constexpr int kMaxK = EDIT_MAX_K;
 constexpr int kMaxPairs = kMaxK * (kMaxK + 1) / 2;
 

@@ -461,20 +461,21 @@ __device__ __forceinline__ void update_vector(float* theta, float* mom, const Mu
   for (int j = 0; j < K; ++j) st16<NT>(reinterpret_cast<u32x4*>(reps.p[j]) + v, out);
 }
 
-// One 16-byte vector of every buffer per thread, one block per 256 vectors,
+// One 16-byte vector of every buffer per thread, one block per 128 vectors,
 // blocks taken from the unit's end: the hardware dispatcher then keeps the
 // in-flight window of each of the 2K+4 streams short and ordered (measured
-// 5.5 TB/s here against 4.9 TB/s for a persistent grid-stride loop), and the
-// first blocks read what pass 1 read last, still in the Infinity Cache.
+// 5.5 TB/s here against 4.9 TB/s for a persistent grid-stride loop; 128-
+// thread blocks edged out 256), and the first blocks read what pass 1 read
+// last, still in the Infinity Cache.
 template <int K, bool BF16, bool NT>
-__global__ __launch_bounds__(kThreads) void pass2_update_kernel(float* __restrict__ theta,
+__global__ __launch_bounds__(kPass2Threads) void pass2_update_kernel(float* __restrict__ theta,
                                                                 float* __restrict__ mom,
                                                                 MutPtrs<K> reps,
                                                                 const UnitRecord* __restrict__ rec,
                                                                 int64_t nvec, int64_t n, double lr,
                                                                 double rho) {
   constexpr int VE = Vec<BF16>::VE;
-  const int64_t v = static_cast<int64_t>(gridDim.x - 1 - blockIdx.x) * kThreads + threadIdx.x;
+  const int64_t v = static_cast<int64_t>(gridDim.x - 1 - blockIdx.x) * kPass2Threads + threadIdx.x;
   const int64_t tail = nvec * VE + threadIdx.x;
   const bool do_tail = blockIdx.x == 0 && tail < n;
 
@@ -590,7 +591,7 @@ hipError_t pass2_launch(int blocks, float* theta, float* mom, void* const* reps,
   MutPtrs<K> rp;
   for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
   const int64_t nvec = n / Vec<BF16>::VE;
-  hipLaunchKernelGGL((pass2_update_kernel<K, BF16, kNT2>), dim3(blocks), dim3(kThreads), 0, stream,
+  hipLaunchKernelGGL((pass2_update_kernel<K, BF16, kNT2>), dim3(blocks), dim3(kPass2Threads), 0, stream,
                      theta, mom, rp, rec, nvec, n, lr, rho);
   return hipGetLastError();
 }

@@ -51,7 +51,7 @@ struct edit_outer {
   int device = 0;
   int num_cu = 0;
   int cap1 = 1;            // resident blocks of pass 1 on the whole GPU
-  bool profiling = false;
+  int32_t profile_every = 0;  // record kernel events on units l with l % every == 0
   char* arena = nullptr;   // one device allocation for every unit's scratch
   std::vector<Unit> units;
 };
@@ -158,11 +158,11 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
     const int64_t nvec = u.n / ve;
     u.rows = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(h->cap1, ceil_div(nvec, kThreads))));
     // pass 2: one vector per thread (block count grows with the unit)
-    if (ceil_div(nvec, kThreads) > INT32_MAX) {
+    if (ceil_div(nvec, kPass2Threads) > INT32_MAX) {
       delete h;
       return fail(EDIT_EINVAL, "layer_numel[" + std::to_string(l) + "] is too large");
     }
-    u.blocks2 = static_cast<int>(std::max<int64_t>(1, ceil_div(nvec, kThreads)));
+    u.blocks2 = static_cast<int>(std::max<int64_t>(1, ceil_div(nvec, kPass2Threads)));
     offs[l] = total;
     const size_t part_bytes = (size_t(num_pairs(K)) * u.rows * sizeof(double) + 255) & ~size_t(255);
     total += rec_bytes + part_bytes;
@@ -239,7 +239,7 @@ edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta,
   prm.flags = h->cfg.flags;
 
   hipError_t e = hipSuccess;
-  const bool prof = h->profiling;
+  const bool prof = h->profile_every > 0 && layer % h->profile_every == 0;
   if (prof) {
     for (hipEvent_t& ev : u.prof)
       if (!ev && (e = hipEventCreate(&ev)) != hipSuccess) return fail_hip(e, "hipEventCreate");
@@ -334,9 +334,10 @@ void edit_outer_destroy(edit_outer_t h) {
   delete h;
 }
 
-edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t enable) {
+edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t every) {
   if (!h) return fail(EDIT_EINVAL, "NULL handle");
-  h->profiling = enable != 0;
+  if (every < 0) return fail(EDIT_EINVAL, "every must be >= 0");
+  h->profile_every = every;
   return EDIT_OK;
 }
 

@@ -294,8 +294,9 @@ class EditOuter:
                    "edit_outer_state_set")
 
     # -- measurement ------------------------------------------------------------
-    def set_profiling(self, enable: bool) -> None:
-        _check(self._lib.edit_outer_set_profiling(self._h, int(bool(enable))), "set_profiling")
+    def set_profiling(self, every: int) -> None:
+        """Record kernel events on units l with l % every == 0 (0: off)."""
+        _check(self._lib.edit_outer_set_profiling(self._h, int(every)), "set_profiling")
 
     def kernel_times(self, layer: int) -> tuple:
         """(pass-1 ms incl. the decision, pass-2 ms) of the unit's last profiled step."""
