@@ -335,29 +335,18 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
 
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
   int64_t v = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
-  if constexpr (K <= 8) {
-    // Double-buffered grid-stride loop: buffer A holds trip t, B trip t+1.
-    float thA[VE], thB[VE];
-    u32x4 rA[K], rB[K];
-    load_pass1<K, BF16, NT>(theta, reps, v, nvec, thA, rA);
-    while (v < nvec) {
-      load_pass1<K, BF16, NT>(theta, reps, v + stride, nvec, thB, rB);
-      gram_vector<K, BF16>(acc, rA, thA);
-      v += stride;
-      if (v >= nvec) break;
-      load_pass1<K, BF16, NT>(theta, reps, v + stride, nvec, thA, rA);
-      gram_vector<K, BF16>(acc, rB, thB);
-      v += stride;
-    }
-  } else {
-    // K > 8: the K(K+1)/2 fp64 accumulators leave no registers for a
-    // second buffer.
-    for (; v < nvec; v += stride) {
-      float th[VE];
-      u32x4 raw[K];
-      load_pass1<K, BF16, NT>(theta, reps, v, nvec, th, raw);
-      gram_vector<K, BF16>(acc, raw, th);
-    }
+  // Double-buffered grid-stride loop: buffer A holds trip t, B trip t+1.
+  float thA[VE], thB[VE];
+  u32x4 rA[K], rB[K];
+  load_pass1<K, BF16, NT>(theta, reps, v, nvec, thA, rA);
+  while (v < nvec) {
+    load_pass1<K, BF16, NT>(theta, reps, v + stride, nvec, thB, rB);
+    gram_vector<K, BF16>(acc, rA, thA);
+    v += stride;
+    if (v >= nvec) break;
+    load_pass1<K, BF16, NT>(theta, reps, v + stride, nvec, thA, rA);
+    gram_vector<K, BF16>(acc, rB, thB);
+    v += stride;
   }
 
   // Ragged tail (fewer than VE elements past the last full vector): block 0.
@@ -389,6 +378,149 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
     double s = red[0][p];
 #pragma unroll
     for (int w = 1; w < kThreads / 64; ++w) s += red[w][p];
+    partials[static_cast<int64_t>(p) * rows + blockIdx.x] = s;
+  }
+}
+
+// Pass 1 for 8 < K <= 16: the Gram matrix sum_i d_i d_i^T over the unit's
+// elements is a rank-n update, and with K(K+1)/2 = 136 fp64 sums per lane a
+// VALU version runs out of registers.  v_mfma_f64_16x16x4f64 keeps the whole
+// 16x16 Gram in 4 fp64 registers per lane: lane l holds worker l % 16's
+// pseudo gradient at vector slot l / 16, which is at once the A operand
+// (A[w][s], lane w + 16s) and the B operand (B[s][w], lane w + 16s), so each
+// instruction adds the outer products of 4 elements of all 16 workers.  The
+// result D[i][j] sits in lane j + 16 * (i % 4), register i / 4.  Lanes of
+// workers >= K feed zeros.
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+// Worker w's replica at vector v, and theta element v*VE + w for lanes w < VE
+// (the 16 lanes of a slot then share theta by shuffles rather than each
+// loading the same 32 bytes).  Zero past the last full vector.
+template <bool BF16, bool NT>
+__device__ __forceinline__ void load_mfma(const float* theta, const void* rep, bool active, int w,
+                                          int64_t v, int64_t nvec, u32x4& raw, float& th) {
+  constexpr int VE = Vec<BF16>::VE;
+  raw = u32x4{0u, 0u, 0u, 0u};
+  th = 0.f;
+  if (v < nvec) {
+    if (w < VE) {
+      if constexpr (NT)
+        th = __builtin_nontemporal_load(theta + v * VE + w);
+      else
+        th = theta[v * VE + w];
+    }
+    if (active) raw = ld16<NT>(reinterpret_cast<const u32x4*>(rep) + v);
+  }
+}
+
+// The ragged tail (n - nvec*VE < VE elements), element by element, in slot 0.
+template <bool BF16>
+__device__ __forceinline__ void load_mfma_tail(const float* theta, const void* rep, bool active,
+                                               int w, int slot, int64_t nvec, int64_t n,
+                                               u32x4& raw, float& th) {
+  constexpr int VE = Vec<BF16>::VE;
+  raw = u32x4{0u, 0u, 0u, 0u};
+  th = 0.f;
+  if (slot != 0) return;
+  if (w < VE && nvec * VE + w < n) th = theta[nvec * VE + w];
+  if (!active) return;
+#pragma unroll
+  for (int e = 0; e < VE; ++e) {
+    const int64_t i = nvec * VE + e;
+    if (i < n) {
+      if constexpr (BF16) {
+        const uint32_t h = reinterpret_cast<const uint16_t*>(rep)[i];
+        raw[e >> 1] |= (e & 1) ? (h << 16) : h;
+      } else {
+        raw[e] = __float_as_uint(reinterpret_cast<const float*>(rep)[i]);
+      }
+    }
+  }
+}
+
+template <bool BF16>
+__device__ __forceinline__ void gram_mfma(f64x4& acc0, f64x4& acc1, const u32x4& raw, float th_lane,
+                                          int lane, bool active) {
+#pragma unroll
+  for (int e = 0; e < Vec<BF16>::VE; ++e) {
+    const float th = __shfl(th_lane, (lane & 48) + e, 64);  // every lane takes part
+    const double d = active ? delta64<BF16>(raw, e, th) : 0.0;
+    if (e & 1)
+      acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(d, d, acc1, 0, 0, 0);
+    else
+      acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(d, d, acc0, 0, 0, 0);
+  }
+}
+
+template <int K, bool BF16, bool NT>
+__global__ __launch_bounds__(kThreads) void pass1_gram_mfma_kernel(const float* __restrict__ theta,
+                                                                   ConstPtrs<K> reps, int64_t nvec,
+                                                                   int64_t n,
+                                                                   double* __restrict__ partials) {
+  static_assert(K > 8 && K <= 16, "MFMA Gram pass covers 8 < K <= 16");
+  constexpr int NP = K * (K + 1) / 2;
+  constexpr int VE = Vec<BF16>::VE;
+  constexpr int kWaves = kThreads / 64;
+  constexpr int V = 2;  // vectors per lane per group: a group is 4*V consecutive vectors
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int w = lane & 15;
+  const int slot = lane >> 4;
+  const bool active = w < K;
+  const void* rep = reps.p[0];
+#pragma unroll
+  for (int j = 1; j < K; ++j) rep = (w == j) ? reps.p[j] : rep;
+
+  const int64_t groups = (nvec + 4 * V - 1) / (4 * V);
+  const int64_t wave_stride = static_cast<int64_t>(gridDim.x) * kWaves;
+  auto load = [&](int64_t g, u32x4 (&raw)[V], float (&th)[V]) {
+#pragma unroll
+    for (int u = 0; u < V; ++u)
+      load_mfma<BF16, NT>(theta, rep, active, w, 4 * V * g + 4 * u + slot, nvec, raw[u], th[u]);
+  };
+  auto accumulate = [&](f64x4& a0, f64x4& a1, const u32x4 (&raw)[V], const float (&th)[V]) {
+#pragma unroll
+    for (int u = 0; u < V; ++u) gram_mfma<BF16>(a0, a1, raw[u], th[u], lane, active);
+  };
+  int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  f64x4 acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
+  float thA[V], thB[V];
+  u32x4 rA[V], rB[V];
+  load(g, rA, thA);
+  while (g < groups) {  // double-buffered like the VALU pass
+    load(g + wave_stride, rB, thB);
+    accumulate(acc0, acc1, rA, thA);
+    g += wave_stride;
+    if (g >= groups) break;
+    load(g + wave_stride, rA, thA);
+    accumulate(acc0, acc1, rB, thB);
+    g += wave_stride;
+  }
+  if (blockIdx.x == 0 && wave == 0 && n > nvec * VE) {  // wave-uniform: MFMA needs all lanes
+    u32x4 raw;
+    float th;
+    load_mfma_tail<BF16>(theta, rep, active, w, slot, nvec, n, raw, th);
+    gram_mfma<BF16>(acc0, acc1, raw, th, lane, active);
+  }
+  const f64x4 acc = acc0 + acc1;
+
+  // Block reduction: each wave's 16x16 Gram to LDS, then the four waves in
+  // order for each upper-triangle pair.
+  __shared__ double gsh[kWaves][16][16];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) gsh[wave][slot + 4 * r][w] = acc[r];
+  __syncthreads();
+  const int rows = gridDim.x;
+  for (int p = threadIdx.x; p < NP; p += kThreads) {
+    int j = 0, left = p;
+    while (left >= K - j) {
+      left -= K - j;
+      ++j;
+    }
+    const int k = j + left;
+    double s = gsh[0][j][k];
+#pragma unroll
+    for (int q = 1; q < kWaves; ++q) s += gsh[q][j][k];
     partials[static_cast<int64_t>(p) * rows + blockIdx.x] = s;
   }
 }
@@ -566,14 +698,23 @@ constexpr bool kNTCopy = false;
 
 namespace {
 
+// Pass 1 for this K: VALU accumulators up to K = 8, matrix cores above.
+template <int K, bool BF16>
+constexpr auto pass1_kernel() {
+  if constexpr (K <= 8)
+    return pass1_gram_kernel<K, BF16, kNT1>;
+  else
+    return pass1_gram_mfma_kernel<K, BF16, kNT1>;
+}
+
 template <int K, bool BF16>
 hipError_t pass1_launch(int blocks, const float* theta, const void* const* reps, int64_t n,
                         double* partials, hipStream_t stream) {
   ConstPtrs<K> rp;
   for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
   const int64_t nvec = n / Vec<BF16>::VE;
-  hipLaunchKernelGGL((pass1_gram_kernel<K, BF16, kNT1>), dim3(blocks), dim3(kThreads), 0, stream,
-                     theta, rp, nvec, n, partials);
+  hipLaunchKernelGGL((pass1_kernel<K, BF16>()), dim3(blocks), dim3(kThreads), 0, stream, theta, rp,
+                     nvec, n, partials);
   return hipGetLastError();
 }
 
@@ -661,8 +802,7 @@ int pass1_blocks_per_cu(int K, bool bf16) {
   switch (K) {
 #define EDIT_CASE(KK)                                                          \
   case KK:                                                                     \
-    return bf16 ? occupancy(pass1_gram_kernel<KK, true, kNT1>)                 \
-                : occupancy(pass1_gram_kernel<KK, false, kNT1>);
+    return bf16 ? occupancy(pass1_kernel<KK, true>()) : occupancy(pass1_kernel<KK, false>());
     EDIT_FOR_EACH_K(EDIT_CASE)
 #undef EDIT_CASE
     default:

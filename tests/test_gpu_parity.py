@@ -57,7 +57,7 @@ def test_c1_linear_layer_all_rounds():
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("K", [1, 2, 3, 5, 8, 13, 16])
+@pytest.mark.parametrize("K", [1, 2, 3, 5, 8, 9, 11, 13, 16])
 def test_ragged_sizes(K, dtype):
     """Unit sizes around the 16-byte vector and the 256-thread block, K = 1..16."""
     sizes = [0, 1, 7, 8, 9, 255, 2049, 100_003, 1_000_005]
