@@ -246,6 +246,8 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="c3", help="workload: c1..c5")
     ap.add_argument("--streams", type=int, default=1, help="HIP streams for the unit pipeline")
+    ap.add_argument("--per-unit", action="store_true",
+                    help="one edit_outer_step_layer call per unit instead of edit_outer_step_round")
     ap.add_argument("--units", type=int, default=0, help="use only the first N units (0 = all)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--profile-every", type=int, default=6,
@@ -295,6 +297,7 @@ def main(argv=None) -> int:
         units.append((th, torch.zeros_like(th), reps))
     torch.cuda.synchronize()
     streams = [torch.cuda.Stream(device=dev) for _ in range(args.streams)] if args.streams > 1 else None
+    plan = lib.prepare_round(units)  # tensors validated once; each step is one C call
     events = args.profile_every > 0
     lib.set_profiling(args.profile_every)
 
@@ -332,7 +335,13 @@ def main(argv=None) -> int:
         a = torch.cuda.Event(enable_timing=True)
         z = torch.cuda.Event(enable_timing=True)
         a.record()
-        lib.step_round(units, streams=streams)
+        if args.per_unit and streams is None:
+            for u, (th, b, reps) in enumerate(units):
+                lib.step_layer(u, th, b, reps)
+        elif streams is None:
+            plan.run()
+        else:
+            lib.step_round(units, streams=streams)
         z.record()
         torch.cuda.synchronize()
         if not timed:
@@ -388,6 +397,8 @@ def main(argv=None) -> int:
             "replica_dtype": wl.replica_dtype,
             "master_dtype": "f32",
             "streams": args.streams,
+            "entry_point": "edit_outer_step_layer per unit" if args.per_unit else
+                           ("edit_outer_step_round" if args.streams <= 1 else "edit_outer_step_layer, streams"),
             "cache_settle_before_step": not args.no_settle,
             "parallelism": "single GPU, K replicas reduced in HBM",
         },

@@ -115,6 +115,21 @@ edit_status_t edit_outer_init(const edit_outer_config_t *cfg, edit_outer_t *out)
 edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float *theta,
                                     float *momentum, void *const *replicas, void *stream);
 
+/* One outer round: `count` distinct units, stepped in the given (forward)
+ * order on `stream` (the layer-wise synchronization of Sec. 3.1), with the
+ * same results bit for bit as calling edit_outer_step_layer for each of them
+ * in that order.  A large unit is enqueued as pass 1, decision, pass 2 back
+ * to back; a small unit's (pass 1 under 32 MB) one-block decision instead
+ * runs inside the next unit's pass-1 launch, saving its own launch.
+ *   layers   [count] unit indices, each at most once (else EDIT_EINVAL)
+ *   theta    [count] device pointers, as in edit_outer_step_layer
+ *   momentum [count] device pointers
+ *   replicas [count * K] device pointers, unit i's K replicas at i*K
+ * Arguments are checked for every unit before anything is enqueued. */
+edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t *layers,
+                                    float *const *theta, float *const *momentum,
+                                    void *const *replicas, void *stream);
+
 /* Copy unit `layer`'s EMA state and last decision to *out, after waiting for
  * that unit's last enqueued step.  EDIT_ESTATE if the unit never stepped and
  * no state was set. */
@@ -141,8 +156,9 @@ const char *edit_outer_last_error(void);
  * EDIT_EINVAL for every < 0. */
 edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t every);
 
-/* Durations in ms of the last profiled step of `layer`: ms[0] the norm/Gram
- * pass plus the decision kernel, ms[1] the update pass.  Waits for it. */
+/* Durations in ms of the last profiled step of `layer`: ms[0] its norm/Gram
+ * pass plus its decision kernel (in a round: its norm/Gram launch, which also
+ * carries the previous unit's decision), ms[1] its update pass.  Waits for it. */
 edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[2]);
 
 /* Plain device-to-device copy kernel of nbytes (a multiple of 16, 16-byte

@@ -41,9 +41,13 @@ struct DecideParams {
 
 // Launchers (kernels.hip).  All enqueue on `stream` and return the launch
 // status; none synchronises.
-hipError_t launch_pass1(int K, bool bf16, int blocks, const float* theta,
+// Pass 1 over `rows` partial rows; when prev_partials is not null, one more
+// block takes the decision of the previous unit of a round (prev_rows rows,
+// record prev_rec) inside the same launch.
+hipError_t launch_pass1(int K, bool bf16, int rows, const float* theta,
                         const void* const* reps, int64_t n, double* partials,
-                        hipStream_t stream);
+                        const double* prev_partials, int prev_rows, UnitRecord* prev_rec,
+                        const DecideParams& prm, hipStream_t stream);
 hipError_t launch_decide(int K, const double* partials, int rows, UnitRecord* rec,
                          const DecideParams& prm, hipStream_t stream);
 hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom,

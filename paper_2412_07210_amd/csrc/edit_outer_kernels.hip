@@ -166,32 +166,38 @@ __device__ __forceinline__ int pair_index(int K, int j, int k) {  // j <= k
 // ------------------------------------------------------------- decision
 
 constexpr int kDecideThreads = 1024;  // one block; wide so the partial loads overlap
+constexpr int kReduceWaves = 16;      // logical waves of the partial reduction
 
 // Reduce the per-block Gram partials [NP][rows] in a fixed order into
-// gram[NP] (shared memory).  Called by every thread of the decision block.
-template <int K>
+// gram[NP] (shared memory).  Called by every thread of one block of
+// kBlockThreads; the sums (16 logical waves, lane r takes rows r, r+64, ...,
+// then a butterfly) depend on neither the block size nor the unrolling, so a
+// standalone decision kernel and one folded into a pass-1 launch agree bit
+// for bit.
+template <int K, int kBlockThreads, int kUnrollRows>
 __device__ void reduce_partials(const double* partials, int rows, double* gram) {
   constexpr int NP = K * (K + 1) / 2;
-  constexpr int kWaves = kDecideThreads / 64;
-  constexpr int PPW = (NP + kWaves - 1) / kWaves;  // pairs per wave
+  constexpr int PPW = (NP + kReduceWaves - 1) / kReduceWaves;  // pairs per logical wave
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  double s[PPW];
+  for (int vw = wave; vw < kReduceWaves; vw += kBlockThreads / 64) {
+    double s[PPW];
 #pragma unroll
-  for (int q = 0; q < PPW; ++q) s[q] = 0.0;
-#pragma unroll 4
-  for (int r = lane; r < rows; r += 64) {
+    for (int q = 0; q < PPW; ++q) s[q] = 0.0;
+#pragma unroll kUnrollRows
+    for (int r = lane; r < rows; r += 64) {
+#pragma unroll
+      for (int q = 0; q < PPW; ++q) {
+        const int p = vw + kReduceWaves * q;
+        if (p < NP) s[q] += __builtin_nontemporal_load(partials + static_cast<int64_t>(p) * rows + r);
+      }
+    }
 #pragma unroll
     for (int q = 0; q < PPW; ++q) {
-      const int p = wave + kWaves * q;
-      if (p < NP) s[q] += __builtin_nontemporal_load(partials + static_cast<int64_t>(p) * rows + r);
+      const int p = vw + kReduceWaves * q;
+      const double t = wave_sum(s[q]);
+      if (lane == 0 && p < NP) gram[p] = t;
     }
-  }
-#pragma unroll
-  for (int q = 0; q < PPW; ++q) {
-    const int p = wave + kWaves * q;
-    const double t = wave_sum(s[q]);
-    if (lane == 0 && p < NP) gram[p] = t;
   }
 }
 
@@ -285,6 +291,26 @@ __device__ void decide(const double* gram, UnitRecord* rec, const DecideParams& 
 
 // ---------------------------------------------------------------- pass 1
 
+// The decision of the previous unit of a round, taken by block 0 of a pass-1
+// launch (partials == nullptr: none).  The previous unit's pass 1 finished
+// before this launch began, so its partials are visible, and its decision
+// costs no serial time of its own.
+struct PrevDecide {
+  const double* partials;
+  int rows;
+  UnitRecord* rec;
+};
+
+template <int K>
+__device__ void run_prev_decide(const PrevDecide& prev, const DecideParams& prm) {
+  __shared__ double gram[K * (K + 1) / 2];
+  // not unrolled: this code shares the pass-1 kernel's register budget
+  reduce_partials<K, kThreads, 1>(prev.partials, prev.rows, gram);
+  __syncthreads();
+  if (threadIdx.x < 64) decide<K>(gram, prev.rec, prm);
+}
+
+
 // Gram contributions of one 16-byte vector of every replica.
 template <int K, bool BF16>
 __device__ __forceinline__ void gram_vector(double (&acc)[K * (K + 1) / 2], const u32x4 (&raw)[K],
@@ -322,9 +348,17 @@ template <int K, bool BF16, bool NT>
 __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __restrict__ theta,
                                                               ConstPtrs<K> reps, int64_t nvec,
                                                               int64_t n,
-                                                              double* __restrict__ partials) {
+                                                              double* __restrict__ partials,
+                                                              PrevDecide prev, DecideParams prm) {
   constexpr int NP = K * (K + 1) / 2;
   constexpr int VE = Vec<BF16>::VE;
+  const int first = prev.partials ? 1 : 0;  // block 0 may take the previous unit's decision
+  if (first && blockIdx.x == 0) {
+    run_prev_decide<K>(prev, prm);
+    return;
+  }
+  const int b = static_cast<int>(blockIdx.x) - first;  // this block's partial row
+  const int rows = static_cast<int>(gridDim.x) - first;
   // fp64 products and sums: on CDNA3/4 a v_fma_f64 issues at the rate of an
   // unpacked v_fma_f32, so exactness costs no extra VALU cycles, and the
   // Gram identity for ||sum_j w_j Delta_j|| stays accurate even when the
@@ -333,8 +367,8 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
 #pragma unroll
   for (int p = 0; p < NP; ++p) acc[p] = 0.0;
 
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
-  int64_t v = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+  const int64_t stride = static_cast<int64_t>(rows) * kThreads;
+  int64_t v = static_cast<int64_t>(b) * kThreads + threadIdx.x;
   // Double-buffered grid-stride loop: buffer A holds trip t, B trip t+1.
   float thA[VE], thB[VE];
   u32x4 rA[K], rB[K];
@@ -349,9 +383,9 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
     v += stride;
   }
 
-  // Ragged tail (fewer than VE elements past the last full vector): block 0.
+  // Ragged tail (fewer than VE elements past the last full vector): row 0.
   const int64_t i = nvec * VE + threadIdx.x;
-  if (blockIdx.x == 0 && i < n) {
+  if (b == 0 && i < n) {
     double d[K];
     const double th = theta[i];
 #pragma unroll
@@ -373,12 +407,11 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
     if (lane == 0) red[wave][p] = s;
   }
   __syncthreads();
-  const int rows = gridDim.x;
   for (int p = threadIdx.x; p < NP; p += kThreads) {
     double s = red[0][p];
 #pragma unroll
     for (int w = 1; w < kThreads / 64; ++w) s += red[w][p];
-    partials[static_cast<int64_t>(p) * rows + blockIdx.x] = s;
+    partials[static_cast<int64_t>(p) * rows + b] = s;
   }
 }
 
@@ -456,8 +489,17 @@ template <int K, bool BF16, bool NT>
 __global__ __launch_bounds__(kThreads) void pass1_gram_mfma_kernel(const float* __restrict__ theta,
                                                                    ConstPtrs<K> reps, int64_t nvec,
                                                                    int64_t n,
-                                                                   double* __restrict__ partials) {
+                                                                   double* __restrict__ partials,
+                                                                   PrevDecide prev,
+                                                                   DecideParams prm) {
   static_assert(K > 8 && K <= 16, "MFMA Gram pass covers 8 < K <= 16");
+  const int first = prev.partials ? 1 : 0;  // block 0 may take the previous unit's decision
+  if (first && blockIdx.x == 0) {
+    run_prev_decide<K>(prev, prm);
+    return;
+  }
+  const int b = static_cast<int>(blockIdx.x) - first;  // this block's partial row
+  const int rows = static_cast<int>(gridDim.x) - first;
   constexpr int NP = K * (K + 1) / 2;
   constexpr int VE = Vec<BF16>::VE;
   constexpr int kWaves = kThreads / 64;
@@ -472,7 +514,7 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_mfma_kernel(const float* 
   for (int j = 1; j < K; ++j) rep = (w == j) ? reps.p[j] : rep;
 
   const int64_t groups = (nvec + 4 * V - 1) / (4 * V);
-  const int64_t wave_stride = static_cast<int64_t>(gridDim.x) * kWaves;
+  const int64_t wave_stride = static_cast<int64_t>(rows) * kWaves;
   auto load = [&](int64_t g, u32x4 (&raw)[V], float (&th)[V]) {
 #pragma unroll
     for (int u = 0; u < V; ++u)
@@ -482,7 +524,7 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_mfma_kernel(const float* 
 #pragma unroll
     for (int u = 0; u < V; ++u) gram_mfma<BF16>(a0, a1, raw[u], th[u], lane, active);
   };
-  int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  int64_t g = static_cast<int64_t>(b) * kWaves + wave;
   f64x4 acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
   float thA[V], thB[V];
   u32x4 rA[V], rB[V];
@@ -496,7 +538,7 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_mfma_kernel(const float* 
     accumulate(acc0, acc1, rB, thB);
     g += wave_stride;
   }
-  if (blockIdx.x == 0 && wave == 0 && n > nvec * VE) {  // wave-uniform: MFMA needs all lanes
+  if (b == 0 && wave == 0 && n > nvec * VE) {  // wave-uniform: MFMA needs all lanes
     u32x4 raw;
     float th;
     load_mfma_tail<BF16>(theta, rep, active, w, slot, nvec, n, raw, th);
@@ -510,7 +552,6 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_mfma_kernel(const float* 
 #pragma unroll
   for (int r = 0; r < 4; ++r) gsh[wave][slot + 4 * r][w] = acc[r];
   __syncthreads();
-  const int rows = gridDim.x;
   for (int p = threadIdx.x; p < NP; p += kThreads) {
     int j = 0, left = p;
     while (left >= K - j) {
@@ -521,7 +562,7 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_mfma_kernel(const float* 
     double s = gsh[0][j][k];
 #pragma unroll
     for (int q = 1; q < kWaves; ++q) s += gsh[q][j][k];
-    partials[static_cast<int64_t>(p) * rows + blockIdx.x] = s;
+    partials[static_cast<int64_t>(p) * rows + b] = s;
   }
 }
 
@@ -532,7 +573,7 @@ __global__ __launch_bounds__(kDecideThreads) void decide_kernel(const double* __
                                                                 int rows, UnitRecord* __restrict__ rec,
                                                                 DecideParams prm) {
   __shared__ double gram[K * (K + 1) / 2];
-  reduce_partials<K>(partials, rows, gram);
+  reduce_partials<K, kDecideThreads, 4>(partials, rows, gram);
   __syncthreads();
   if (threadIdx.x < 64) decide<K>(gram, rec, prm);
 }
@@ -708,13 +749,16 @@ constexpr auto pass1_kernel() {
 }
 
 template <int K, bool BF16>
-hipError_t pass1_launch(int blocks, const float* theta, const void* const* reps, int64_t n,
-                        double* partials, hipStream_t stream) {
+hipError_t pass1_launch(int rows, const float* theta, const void* const* reps, int64_t n,
+                        double* partials, const double* prev_partials, int prev_rows,
+                        UnitRecord* prev_rec, const DecideParams& prm, hipStream_t stream) {
   ConstPtrs<K> rp;
   for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
   const int64_t nvec = n / Vec<BF16>::VE;
+  const PrevDecide prev{prev_partials, prev_rows, prev_rec};
+  const int blocks = rows + (prev_partials ? 1 : 0);
   hipLaunchKernelGGL((pass1_kernel<K, BF16>()), dim3(blocks), dim3(kThreads), 0, stream, theta, rp,
-                     nvec, n, partials);
+                     nvec, n, partials, prev, prm);
   return hipGetLastError();
 }
 
@@ -751,13 +795,16 @@ int occupancy(Kern kernel) {
 #define EDIT_FOR_EACH_K(X) \
   X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16)
 
-hipError_t launch_pass1(int K, bool bf16, int blocks, const float* theta, const void* const* reps,
-                        int64_t n, double* partials, hipStream_t stream) {
+hipError_t launch_pass1(int K, bool bf16, int rows, const float* theta, const void* const* reps,
+                        int64_t n, double* partials, const double* prev_partials, int prev_rows,
+                        UnitRecord* prev_rec, const DecideParams& prm, hipStream_t stream) {
   switch (K) {
-#define EDIT_CASE(KK)                                                                    \
-  case KK:                                                                               \
-    return bf16 ? pass1_launch<KK, true>(blocks, theta, reps, n, partials, stream)       \
-                : pass1_launch<KK, false>(blocks, theta, reps, n, partials, stream);
+#define EDIT_CASE(KK)                                                                       \
+  case KK:                                                                                  \
+    return bf16 ? pass1_launch<KK, true>(rows, theta, reps, n, partials, prev_partials,     \
+                                         prev_rows, prev_rec, prm, stream)                  \
+                : pass1_launch<KK, false>(rows, theta, reps, n, partials, prev_partials,    \
+                                          prev_rows, prev_rec, prm, stream);
     EDIT_FOR_EACH_K(EDIT_CASE)
 #undef EDIT_CASE
     default:

@@ -2,9 +2,11 @@
 //
 // A handle owns, per sync unit: the device record (EMA state + decision),
 // the per-block Gram partials of pass 1, a completion event and (when
-// profiling) three timing events.  A step validates its arguments, enqueues
-// pass1 -> decide -> pass2 on the caller's stream and returns; there is no
-// host synchronisation on the step path and no device-to-host traffic.
+// profiling) four timing events.  A step validates its arguments, enqueues
+// pass1 -> decide -> pass2 on the caller's stream and returns; a round
+// enqueues many units with each unit's decision folded into the next unit's
+// pass-1 launch.  There is no host synchronisation on the step path and no
+// device-to-host traffic.
 #include <climits>
 #include <cmath>
 #include <cstdio>
@@ -37,7 +39,7 @@ struct Unit {
   double* partials = nullptr;
   UnitRecord* rec = nullptr;
   hipEvent_t done = nullptr;
-  hipEvent_t prof[3] = {nullptr, nullptr, nullptr};
+  hipEvent_t prof[4] = {nullptr, nullptr, nullptr, nullptr};
   bool pending = false;   // `done` has been recorded at least once
   bool profiled = false;  // prof[] hold the last step's timestamps
   bool has_state = false; // stepped or state_set at least once
@@ -156,7 +158,11 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
     Unit& u = h->units[l];
     u.n = h->numel[l];
     const int64_t nvec = u.n / ve;
-    u.rows = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(h->cap1, ceil_div(nvec, kThreads))));
+    // one resident slot stays free for the block that takes the previous
+    // unit's decision in a round (and step_layer uses the same rows, so both
+    // paths reduce in the same order)
+    u.rows = static_cast<int>(
+        std::max<int64_t>(1, std::min<int64_t>(h->cap1 - 1, ceil_div(nvec, kThreads))));
     // pass 2: one vector per thread (block count grows with the unit)
     if (ceil_div(nvec, kPass2Threads) > INT32_MAX) {
       delete h;
@@ -189,47 +195,46 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
   return EDIT_OK;
 }
 
-edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta, float* momentum,
-                                    void* const* replicas, void* stream) {
-  if (!h) return fail(EDIT_EINVAL, "NULL handle");
+}  // extern "C"
+
+namespace {
+
+// Argument checks shared by step_layer and step_round.
+edit_status_t check_step(const edit_outer* h, int32_t layer, const float* theta,
+                         const float* momentum, void* const* replicas) {
   if (layer < 0 || layer >= h->cfg.num_layers)
     return fail(EDIT_EINVAL, "layer " + std::to_string(layer) + " out of range");
-  Unit& u = h->units[layer];
+  const Unit& u = h->units[layer];
   const int K = h->cfg.num_workers;
-  const bool bf16 = h->cfg.replica_dtype == EDIT_BF16;
   const int64_t n = u.n;
-  if (!replicas && n > 0) return fail(EDIT_EINVAL, "replicas must not be NULL");
-  if (n > 0) {
-    if (!theta || !momentum) return fail(EDIT_EINVAL, "theta and momentum must not be NULL");
-    if (!aligned16(theta) || !aligned16(momentum))
-      return fail(EDIT_EINVAL, "theta and momentum must be 16-byte aligned");
-    // Every buffer's byte range, for the alias check.
-    struct Range { uintptr_t lo, hi; };
-    Range r[EDIT_MAX_K + 2];
-    r[0] = {reinterpret_cast<uintptr_t>(theta), reinterpret_cast<uintptr_t>(theta) + 4 * n};
-    r[1] = {reinterpret_cast<uintptr_t>(momentum), reinterpret_cast<uintptr_t>(momentum) + 4 * n};
-    const int64_t rb = bf16 ? 2 : 4;
-    for (int j = 0; j < K; ++j) {
-      if (!replicas[j]) return fail(EDIT_EINVAL, "replica pointer " + std::to_string(j) + " is NULL");
-      if (!aligned16(replicas[j]))
-        return fail(EDIT_EINVAL, "replica " + std::to_string(j) + " is not 16-byte aligned");
-      const uintptr_t p = reinterpret_cast<uintptr_t>(replicas[j]);
-      r[2 + j] = {p, p + rb * n};
-    }
-    for (int a = 0; a < K + 2; ++a)
-      for (int b = a + 1; b < K + 2; ++b)
-        if (r[a].lo < r[b].hi && r[b].lo < r[a].hi)
-          return fail(EDIT_EINVAL, "theta, momentum and the replicas must not overlap");
+  if (n == 0) return EDIT_OK;
+  if (!replicas) return fail(EDIT_EINVAL, "replicas must not be NULL");
+  if (!theta || !momentum) return fail(EDIT_EINVAL, "theta and momentum must not be NULL");
+  if (!aligned16(theta) || !aligned16(momentum))
+    return fail(EDIT_EINVAL, "theta and momentum must be 16-byte aligned");
+  // Every buffer's byte range, for the alias check.
+  struct Range {
+    uintptr_t lo, hi;
+  };
+  Range r[EDIT_MAX_K + 2];
+  r[0] = {reinterpret_cast<uintptr_t>(theta), reinterpret_cast<uintptr_t>(theta) + 4 * n};
+  r[1] = {reinterpret_cast<uintptr_t>(momentum), reinterpret_cast<uintptr_t>(momentum) + 4 * n};
+  const int64_t rb = h->cfg.replica_dtype == EDIT_BF16 ? 2 : 4;
+  for (int j = 0; j < K; ++j) {
+    if (!replicas[j]) return fail(EDIT_EINVAL, "replica pointer " + std::to_string(j) + " is NULL");
+    if (!aligned16(replicas[j]))
+      return fail(EDIT_EINVAL, "replica " + std::to_string(j) + " is not 16-byte aligned");
+    const uintptr_t p = reinterpret_cast<uintptr_t>(replicas[j]);
+    r[2 + j] = {p, p + rb * n};
   }
-  edit_status_t st = check_device(h);
-  if (st != EDIT_OK) return st;
+  for (int a = 0; a < K + 2; ++a)
+    for (int b = a + 1; b < K + 2; ++b)
+      if (r[a].lo < r[b].hi && r[b].lo < r[a].hi)
+        return fail(EDIT_EINVAL, "theta, momentum and the replicas must not overlap");
+  return EDIT_OK;
+}
 
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const void* const* creps = const_cast<const void* const*>(replicas);
-  static void* const kNoReplicas[EDIT_MAX_K] = {};
-  if (n == 0) creps = kNoReplicas;
-  void* const* mreps = n == 0 ? kNoReplicas : replicas;
-
+DecideParams decide_params(const edit_outer* h) {
   DecideParams prm;
   prm.alpha = h->cfg.ema_alpha;
   prm.delta = h->cfg.z_threshold;
@@ -237,27 +242,150 @@ edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta,
   prm.eps = h->cfg.clip_eps;
   prm.warmup = h->cfg.ema_warmup_rounds;
   prm.flags = h->cfg.flags;
+  return prm;
+}
 
-  hipError_t e = hipSuccess;
-  const bool prof = h->profile_every > 0 && layer % h->profile_every == 0;
-  if (prof) {
-    for (hipEvent_t& ev : u.prof)
-      if (!ev && (e = hipEventCreate(&ev)) != hipSuccess) return fail_hip(e, "hipEventCreate");
-    if ((e = hipEventRecord(u.prof[0], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+static void* const kNoReplicas[EDIT_MAX_K] = {};
+
+// Units whose pass 1 reads less than this fold their decision into the next
+// pass-1 launch of a round (see edit_outer_step_round).
+constexpr int64_t kSmallUnitBytes = 32ll << 20;
+
+// Enqueue helpers; each returns EDIT_OK or the failure (message already set).
+struct Enqueue {
+  edit_outer* h;
+  hipStream_t s;
+  DecideParams prm;
+  int K;
+  bool bf16;
+
+  bool profiled(int32_t layer) const {
+    return h->profile_every > 0 && layer % h->profile_every == 0;
   }
-  e = launch_pass1(K, bf16, u.rows, theta, creps, n, u.partials, s);
-  if (e != hipSuccess) return fail_hip(e, "pass1 launch");
-  e = launch_decide(K, u.partials, u.rows, u.rec, prm, s);
-  if (e != hipSuccess) return fail_hip(e, "decide launch");
-  if (prof && (e = hipEventRecord(u.prof[1], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
-  e = launch_pass2(K, bf16, u.blocks2, theta, momentum, mreps, u.rec, n, h->cfg.outer_lr,
-                   h->cfg.momentum, s);
-  if (e != hipSuccess) return fail_hip(e, "pass2 launch");
-  if (prof && (e = hipEventRecord(u.prof[2], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
-  if ((e = hipEventRecord(u.done, s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
-  u.pending = true;
-  u.profiled = prof;
-  u.has_state = true;
+  edit_status_t event(Unit& u, int32_t layer, int k) {
+    if (!profiled(layer)) return EDIT_OK;
+    hipError_t e = hipSuccess;
+    if (!u.prof[k] && (e = hipEventCreate(&u.prof[k])) != hipSuccess)
+      return fail_hip(e, "hipEventCreate");
+    if ((e = hipEventRecord(u.prof[k], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+    return EDIT_OK;
+  }
+  // pass 1 of `layer`, optionally with the decision of `prev` in the same launch
+  edit_status_t pass1(int32_t layer, const float* theta, void* const* replicas, Unit* prev) {
+    Unit& u = h->units[layer];
+    const void* const* creps =
+        u.n == 0 ? kNoReplicas : const_cast<const void* const*>(replicas);
+    hipError_t e = launch_pass1(K, bf16, u.rows, theta, creps, u.n, u.partials,
+                                prev ? prev->partials : nullptr, prev ? prev->rows : 0,
+                                prev ? prev->rec : nullptr, prm, s);
+    return e == hipSuccess ? EDIT_OK : fail_hip(e, "pass1 launch");
+  }
+  edit_status_t decide(int32_t layer) {
+    Unit& u = h->units[layer];
+    hipError_t e = launch_decide(K, u.partials, u.rows, u.rec, prm, s);
+    return e == hipSuccess ? EDIT_OK : fail_hip(e, "decide launch");
+  }
+  edit_status_t pass2(int32_t layer, float* theta, float* momentum, void* const* replicas) {
+    Unit& u = h->units[layer];
+    void* const* mreps = u.n == 0 ? kNoReplicas : replicas;
+    hipError_t e = launch_pass2(K, bf16, u.blocks2, theta, momentum, mreps, u.rec, u.n,
+                                h->cfg.outer_lr, h->cfg.momentum, s);
+    if (e != hipSuccess) return fail_hip(e, "pass2 launch");
+    return EDIT_OK;
+  }
+  edit_status_t finish(int32_t layer) {
+    Unit& u = h->units[layer];
+    hipError_t e = hipEventRecord(u.done, s);
+    if (e != hipSuccess) return fail_hip(e, "hipEventRecord");
+    u.pending = true;
+    u.profiled = profiled(layer);
+    u.has_state = true;
+    return EDIT_OK;
+  }
+};
+
+#define EDIT_TRY(expr)                    \
+  do {                                    \
+    const edit_status_t st_ = (expr);     \
+    if (st_ != EDIT_OK) return st_;       \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta, float* momentum,
+                                    void* const* replicas, void* stream) {
+  if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  EDIT_TRY(check_step(h, layer, theta, momentum, replicas));
+  EDIT_TRY(check_device(h));
+  Enqueue q{h, reinterpret_cast<hipStream_t>(stream), decide_params(h), h->cfg.num_workers,
+            h->cfg.replica_dtype == EDIT_BF16};
+  EDIT_TRY(q.event(h->units[layer], layer, 0));
+  EDIT_TRY(q.pass1(layer, theta, replicas, nullptr));
+  EDIT_TRY(q.decide(layer));
+  EDIT_TRY(q.event(h->units[layer], layer, 1));
+  EDIT_TRY(q.event(h->units[layer], layer, 2));
+  EDIT_TRY(q.pass2(layer, theta, momentum, replicas));
+  EDIT_TRY(q.event(h->units[layer], layer, 3));
+  return q.finish(layer);
+}
+
+edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t* layers,
+                                    float* const* theta, float* const* momentum,
+                                    void* const* replicas, void* stream) {
+  if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  if (count < 1) return fail(EDIT_EINVAL, "count must be >= 1");
+  if (!layers || !theta || !momentum || !replicas)
+    return fail(EDIT_EINVAL, "layers, theta, momentum and replicas must not be NULL");
+  const int K = h->cfg.num_workers;
+  std::vector<char> seen(h->cfg.num_layers, 0);
+  for (int32_t i = 0; i < count; ++i) {
+    EDIT_TRY(check_step(h, layers[i], theta[i], momentum[i], replicas + static_cast<size_t>(i) * K));
+    if (seen[layers[i]]++)
+      return fail(EDIT_EINVAL, "layer " + std::to_string(layers[i]) + " appears twice in a round");
+  }
+  EDIT_TRY(check_device(h));
+  Enqueue q{h, reinterpret_cast<hipStream_t>(stream), decide_params(h), K,
+            h->cfg.replica_dtype == EDIT_BF16};
+  // A large unit runs p1 -> decide -> p2 back to back: its pass 2 walks the
+  // unit from the end and finds what pass 1 read last still in the Infinity
+  // Cache, which is worth more than the decision's launch.  A small unit's
+  // decision instead rides in the next pass-1 launch (one extra block), and
+  // its pass 2 follows that launch; the last pending decision runs alone.
+  const int64_t rbytes = h->cfg.replica_dtype == EDIT_BF16 ? 2 : 4;
+  int32_t pending = -1;  // index i of a small unit whose decision is not launched yet
+  auto flush_pass2 = [&](int32_t i) -> edit_status_t {
+    const int32_t l = layers[i];
+    void* const* reps = replicas + static_cast<size_t>(i) * K;
+    EDIT_TRY(q.event(h->units[l], l, 2));
+    EDIT_TRY(q.pass2(l, theta[i], momentum[i], reps));
+    EDIT_TRY(q.event(h->units[l], l, 3));
+    return q.finish(l);
+  };
+  for (int32_t i = 0; i < count; ++i) {
+    const int32_t l = layers[i];
+    Unit& u = h->units[l];
+    Unit* prev = pending >= 0 ? &h->units[layers[pending]] : nullptr;
+    EDIT_TRY(q.event(u, l, 0));
+    EDIT_TRY(q.pass1(l, theta[i], replicas + static_cast<size_t>(i) * K, prev));
+    if (pending >= 0) {
+      EDIT_TRY(flush_pass2(pending));
+      pending = -1;
+    }
+    if (u.n * (K * rbytes + 4) < kSmallUnitBytes) {
+      EDIT_TRY(q.event(u, l, 1));
+      pending = i;
+    } else {
+      EDIT_TRY(q.decide(l));
+      EDIT_TRY(q.event(u, l, 1));
+      EDIT_TRY(flush_pass2(i));
+    }
+  }
+  if (pending >= 0) {
+    EDIT_TRY(q.decide(layers[pending]));
+    EDIT_TRY(flush_pass2(pending));
+  }
   return EDIT_OK;
 }
 
@@ -347,11 +475,11 @@ edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[2]
     return fail(EDIT_EINVAL, "layer " + std::to_string(layer) + " out of range");
   Unit& u = h->units[layer];
   if (!u.profiled) return fail(EDIT_ESTATE, "the unit's last step was not profiled");
-  hipError_t e = hipEventSynchronize(u.prof[2]);
+  hipError_t e = hipEventSynchronize(u.prof[3]);
   if (e != hipSuccess) return fail_hip(e, "hipEventSynchronize");
-  for (int k = 0; k < 2; ++k)
-    if ((e = hipEventElapsedTime(&ms[k], u.prof[k], u.prof[k + 1])) != hipSuccess)
-      return fail_hip(e, "hipEventElapsedTime");
+  if ((e = hipEventElapsedTime(&ms[0], u.prof[0], u.prof[1])) != hipSuccess ||
+      (e = hipEventElapsedTime(&ms[1], u.prof[2], u.prof[3])) != hipSuccess)
+    return fail_hip(e, "hipEventElapsedTime");
   return EDIT_OK;
 }
 

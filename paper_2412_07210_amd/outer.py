@@ -27,7 +27,8 @@ EDIT_OK, EDIT_EINVAL, EDIT_ENOMEM, EDIT_EHIP, EDIT_ESTATE, EDIT_ENODEV = 0, -1, 
 
 # Every function the header declares; the CPU tests check the library exports them.
 EXPORTS = (
-    "edit_outer_init", "edit_outer_step_layer", "edit_outer_state_get", "edit_outer_state_set",
+    "edit_outer_init", "edit_outer_step_layer", "edit_outer_step_round",
+    "edit_outer_state_get", "edit_outer_state_set",
     "edit_outer_destroy", "edit_outer_strerror", "edit_outer_last_error",
     "edit_outer_set_profiling", "edit_outer_kernel_times", "edit_outer_copy_probe",
 )
@@ -91,6 +92,10 @@ def load_library() -> ctypes.CDLL:
     lib.edit_outer_init.restype = st
     lib.edit_outer_step_layer.argtypes = [vp, ctypes.c_int32, vp, vp, ctypes.POINTER(vp), vp]
     lib.edit_outer_step_layer.restype = st
+    lib.edit_outer_step_round.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
+                                          ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                          ctypes.POINTER(vp), vp]
+    lib.edit_outer_step_round.restype = st
     lib.edit_outer_state_get.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(_LayerState)]
     lib.edit_outer_state_get.restype = st
     lib.edit_outer_state_set.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(_LayerState)]
@@ -242,20 +247,29 @@ class EditOuter:
                                                      _stream_handle(stream, self.device))
         _check(status, "edit_outer_step_layer")
 
+    def prepare_round(self, units: Sequence[tuple],
+                      layers: Optional[Sequence[int]] = None) -> "RoundPlan":
+        """Validate a round's tensors once; RoundPlan.run() then enqueues it
+        with a single edit_outer_step_round call (no per-tensor Python work)."""
+        return RoundPlan(self, units, layers)
+
     def step_round(self, units: Sequence[tuple], streams: Optional[List[torch.cuda.Stream]] = None,
                    layers: Optional[Sequence[int]] = None) -> None:
-        """Step every unit in forward order; unit l goes to streams[l % S].
+        """Step every unit in forward order.
 
-        units[l] = (theta, momentum, replicas).  The streams start after the
-        current stream's pending work and the current stream waits for all of
-        them, so the round is ordered like a single call on the current stream.
+        units[i] = (theta, momentum, replicas) of unit layers[i] (default i).
+        Without `streams` this is one edit_outer_step_round call on the
+        current stream.  With streams, unit i goes to streams[i % S] through
+        edit_outer_step_layer; the streams start after the current stream's
+        pending work and the current stream waits for all of them.
         """
-        cur = torch.cuda.current_stream(self.device)
         layers = list(range(len(units))) if layers is None else list(layers)
         if not streams:
-            for l, (th, b, reps) in zip(layers, units):
-                self.step_layer(l, th, b, reps, stream=cur)
+            RoundPlan(self, units, layers).run()
             return
+        if len(layers) != len(units):
+            raise ValueError("layers and units differ in length")
+        cur = torch.cuda.current_stream(self.device)
         start = torch.cuda.Event()
         start.record(cur)
         for s in streams:
@@ -304,6 +318,51 @@ class EditOuter:
         with torch.cuda.device(self.device):
             _check(self._lib.edit_outer_kernel_times(self._h, int(layer), ms), "kernel_times")
         return float(ms[0]), float(ms[1])
+
+
+class RoundPlan:
+    """A validated round: the units' tensors checked once, their device
+    pointers marshalled once.  The plan keeps the tensors alive; their storage
+    must not be reallocated while the plan is used."""
+
+    def __init__(self, handle: EditOuter, units: Sequence[tuple],
+                 layers: Optional[Sequence[int]] = None):
+        layers = list(range(len(units))) if layers is None else list(layers)
+        if len(layers) != len(units) or not units:
+            raise ValueError("need one layer index per unit and at least one unit")
+        K = handle.cfg.num_workers
+        c = len(units)
+        self._handle = handle
+        self._units = list(units)
+        self._count = c
+        self._layers = (ctypes.c_int32 * c)(*layers)
+        self._theta = (ctypes.c_void_p * c)()
+        self._mom = (ctypes.c_void_p * c)()
+        self._reps = (ctypes.c_void_p * (c * K))()
+        for i, (l, (t, b, reps)) in enumerate(zip(layers, units)):
+            if not 0 <= l < len(handle._numel):
+                raise IndexError(f"layer {l} out of range")
+            n = handle._numel[l]
+            if len(reps) != K:
+                raise ValueError(f"expected {K} replicas, got {len(reps)}")
+            handle._check_tensor(t, n, torch.float32, "theta")
+            handle._check_tensor(b, n, torch.float32, "momentum")
+            for j, r in enumerate(reps):
+                handle._check_tensor(r, n, handle.cfg.torch_dtype, f"replicas[{j}]")
+                self._reps[i * K + j] = r.data_ptr()
+            self._theta[i], self._mom[i] = t.data_ptr(), b.data_ptr()
+
+    def run(self, stream: Optional[torch.cuda.Stream] = None) -> None:
+        h = self._handle
+        s = _stream_handle(stream, h.device)
+        if torch.cuda.current_device() != h.device.index:
+            with torch.cuda.device(h.device):
+                status = h._lib.edit_outer_step_round(h._h, self._count, self._layers, self._theta,
+                                                      self._mom, self._reps, s)
+        else:
+            status = h._lib.edit_outer_step_round(h._h, self._count, self._layers, self._theta,
+                                                  self._mom, self._reps, s)
+        _check(status, "edit_outer_step_round")
 
 
 def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream: Optional[torch.cuda.Stream] = None) -> None:

@@ -90,6 +90,7 @@ def test_null_arguments_are_rejected():
     h = ctypes.c_void_p()
     assert lib.edit_outer_init(None, ctypes.byref(h)) == outer.EDIT_EINVAL
     assert lib.edit_outer_step_layer(None, 0, None, None, None, None) == outer.EDIT_EINVAL
+    assert lib.edit_outer_step_round(None, 1, None, None, None, None, None) == outer.EDIT_EINVAL
     assert lib.edit_outer_state_get(None, 0, None) == outer.EDIT_EINVAL
     assert lib.edit_outer_copy_probe(None, None, 15, None) == outer.EDIT_EINVAL
     lib.edit_outer_destroy(None)

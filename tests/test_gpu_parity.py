@@ -228,22 +228,54 @@ def test_resume_from_saved_state_is_bitwise():
     s2.close()
 
 
-def test_stream_pipeline_matches_single_stream():
-    """Units issued in forward order over three streams give the same bits as
-    issuing them on one stream."""
-    wl = synth.small("c3", [1_000_000 + 8 * i for i in range(6)], name="pipe")
+@pytest.mark.parametrize("K,dtype", [(8, "bf16"), (4, "f32"), (16, "bf16")])
+def test_round_and_streams_match_unit_by_unit(K, dtype):
+    """A round (each unit's decision folded into the next unit's pass-1 launch)
+    and a 3-stream pipeline give the same bits as unit-by-unit calls, over
+    several rounds (EMA state carried), units of mixed sizes and a unit order
+    that is not the index order."""
+    sizes = [1_000_000, 2048, 7, 3_000_017, 0, 65_536 + 3]
+    wl = synth.small("c3", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=1,
+                     name=f"round{K}{dtype}")
+    order = [2, 0, 5, 1, 4, 3]
     results = []
-    for streams in (None, [torch.cuda.Stream() for _ in range(3)]):
-        h = EditOuter(OuterConfig(wl.num_workers, wl.layer_numel, "bf16"), DEV)
+    for mode in ("layer", "round", "streams"):
+        h = EditOuter(OuterConfig(K, wl.layer_numel, dtype, ema_warmup_rounds=1), DEV)
         units = [_fresh_inputs(wl, u, 0, DEV) for u in range(wl.num_units)]
-        torch.cuda.synchronize()
-        h.step_round(units, streams=streams)
-        torch.cuda.synchronize()
-        results.append(units)
+        for t in range(3):
+            for u in range(wl.num_units):
+                wl.fill_replicas(units[u][0], units[u][2], u, t)
+            torch.cuda.synchronize()
+            ordered = [units[u] for u in order]
+            if mode == "layer":
+                for u in order:
+                    h.step_layer(u, *units[u])
+            elif mode == "round":
+                h.step_round(ordered, layers=order)
+            else:
+                h.step_round(ordered, layers=order, streams=[torch.cuda.Stream() for _ in range(3)])
+            torch.cuda.synchronize()
+        states = [h.state_get(u) for u in range(wl.num_units)]
+        results.append((units, states))
         h.close()
-    for (a, b) in zip(*results):
-        assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
-        assert all(torch.equal(x, y) for x, y in zip(a[2], b[2]))
+    (ua, sa) = results[0]
+    for (ub, sb) in results[1:]:
+        for a, b in zip(ua, ub):
+            assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+            assert all(torch.equal(x, y) for x, y in zip(a[2], b[2]))
+        for x, y in zip(sa, sb):
+            assert np.array_equal(x.norm, y.norm) and np.array_equal(x.ema_mean, y.ema_mean)
+            assert x.round == y.round == 3
+
+
+def test_round_rejects_repeated_unit():
+    wl = synth.small("c3", [4096, 4096], name="rep")
+    h = EditOuter(OuterConfig(wl.num_workers, wl.layer_numel, "bf16"), DEV)
+    units = [_fresh_inputs(wl, u, 0, DEV) for u in range(2)]
+    with pytest.raises(EditOuterError) as e:
+        h.step_round([units[0], units[0]], layers=[0, 0])
+    assert "twice" in str(e.value)
+    h.close()
 
 
 # ------------------------------------------------------------ API errors
