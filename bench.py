@@ -134,10 +134,70 @@ PROFILE_CMDS = {
 
 
 def _kernel_kind(name: str) -> str:
-    for kind in ("pass1_gram_kernel", "decide_kernel", "pass2_update_kernel", "copy_kernel"):
+    for kind in ("pass1_gram_kernel", "pass1_gram_mfma_kernel", "decide_kernel", "pass2_update_kernel",
+                 "copy_kernel"):
         if kind in name:
             return kind
     return ""
+
+
+def summarize_trace_by_grid(out_dir: str, name: str) -> str:
+    """Group a rocprofv3 kernel trace (`<out>/prof_trace_<name>/<name>_kernel_trace.csv`) by
+    kernel and grid size, so units of different sizes in one workload get rows of their own.
+    Streams the CSV (it is large); returns the markdown table written to profiles/."""
+    import csv
+    from paper_2412_07210_amd import synth
+
+    wl = synth.get(name)
+    K, R = wl.num_workers, wl.replica_bytes
+    sizes = sorted(set(wl.layer_numel))
+    groups, regs = {}, {}
+    with open(os.path.join(out_dir, f"prof_trace_{name}", f"{name}_kernel_trace.csv")) as f:
+        for row in csv.DictReader(f):
+            kind = _kernel_kind(row["Kernel_Name"])
+            if not kind or kind == "copy_kernel":
+                continue
+            grid = int(row.get("Grid_Size") or row.get("Grid_Size_X"))
+            dur = int(row["End_Timestamp"]) - int(row["Start_Timestamp"])
+            groups.setdefault((kind, grid), []).append(dur)
+            regs[kind] = (row.get("VGPR_Count", "?"), row.get("Accum_VGPR_Count", "?"),
+                          row.get("LDS_Block_Size", "?"))
+
+    def unit_of(kind, grid):
+        for n in sizes:
+            nvec = -(-n // 8)
+            if kind == "pass2_update_kernel" and -(-nvec // 128) * 128 == grid:
+                return n
+            if kind.startswith("pass1_gram") and -(-nvec // 256) >= grid // 256 - 1:
+                return n
+        return None
+
+    algo = lambda kind, n: {"pass1_gram_kernel": n * (4 + K * R), "pass1_gram_mfma_kernel": n * (4 + K * R),
+                            "pass2_update_kernel": n * (16 + 2 * K * R)}.get(kind)
+    lines = [f"# Kernel durations by unit size: {wl.description}", "",
+             "Command (from the repository root; `<out>` = gpurun_out):", "",
+             f"    rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace_{name} -o {name} -- "
+             f"python bench.py --config {name} --steps 10 --warmup 5 --no-cpu-baseline", "",
+             f"Summarised with `python bench.py --summarize-trace <out> {name}` (groups the trace's "
+             "dispatches by kernel and grid size).", "",
+             "| kernel | grid work-items | unit elements | calls | avg us | min us | max us | "
+             "algorithmic bytes | GB/s at avg |", "|---|---|---|---|---|---|---|---|---|"]
+    for (kind, grid) in sorted(groups, key=lambda kg: (kg[0], -kg[1])):
+        d = groups[(kind, grid)]
+        avg = sum(d) / len(d)
+        n = unit_of(kind, grid)
+        b = algo(kind, n) if n else None
+        gbps = f"{b / (avg * 1e-9) / 1e9:.1f}" if b else "-"
+        lines.append(f"| {kind} | {grid} | {n if n else '-'} | {len(d)} | {avg / 1e3:.1f} | "
+                     f"{min(d) / 1e3:.1f} | {max(d) / 1e3:.1f} | {b if b else '-'} | {gbps} |")
+    lines += ["", "Registers per lane (VGPR, AGPR) and LDS bytes per block, from the same trace:", ""]
+    for kind, (v, a, l) in sorted(regs.items()):
+        lines.append(f"- {kind}: {v} VGPR, {a} AGPR, {l} B LDS")
+    text = "\n".join(lines) + "\n"
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", f"{name}_kernel_trace_by_unit.md"), "w") as f:
+        f.write(text)
+    return text
 
 
 def summarize_profiles(out_dir: str, bench_json: str) -> None:
@@ -259,9 +319,14 @@ def main(argv=None) -> int:
                     help="skip the untimed cache settle between input generation and the step")
     ap.add_argument("--summarize-profiles", nargs=2, metavar=("OUT_DIR", "BENCH_JSON"),
                     help="write profiles/ summaries from rocprofv3 CSVs under OUT_DIR (no GPU)")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("OUT_DIR", "WORKLOAD"),
+                    help="write a per-unit-size kernel table from a rocprofv3 kernel trace (no GPU)")
     args = ap.parse_args(argv)
     if args.summarize_profiles:
         summarize_profiles(*args.summarize_profiles)
+        return 0
+    if args.summarize_trace:
+        print(summarize_trace_by_grid(*args.summarize_trace))
         return 0
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
