@@ -130,6 +130,37 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
                                     float *const *theta, float *const *momentum,
                                     void *const *replicas, void *stream);
 
+/* A module whose parameters are sharded over several devices (the model-shard
+ * group of Sec. 3.1) still takes its penalty on norms of the WHOLE module
+ * (Sec. 3.2): each shard contributes partial sums, which the shards add up
+ * before deciding.  The two calls below split edit_outer_step_layer at that
+ * point.  Each shard is a unit of its own handle (its own layer_numel); the
+ * caller adds the shards' Gram vectors (e.g. an all-reduce) and hands the
+ * same sum to every shard, whose decisions and EMA states then agree bit for
+ * bit.  For an unsplit unit, gram_layer followed by apply_layer with that
+ * Gram gives the same results bit for bit as edit_outer_step_layer.
+ *
+ * The Gram vector holds the K(K+1)/2 sums sum_i Delta_j[i] Delta_k[i] over
+ * the unit's elements, Delta_j = replica_j - theta, for j <= k, row by row:
+ * (0,0), (0,1), ..., (0,K-1), (1,1), ..., (K-1,K-1); fp64, device memory,
+ * 8-byte aligned, owned by the caller.  Its diagonal holds the squared norms
+ * G_j^2, and the norm of the weighted average of Eq. 3 follows from it as
+ * sqrt(w^T Gram w).
+ *
+ * gram_layer: pass 1 of unit `layer` only, enqueued on `stream`; writes
+ *   `gram` and changes no state.  theta and the replicas are only read.
+ * apply_layer: the decision (anomaly test, EMA update, weights, clip) from
+ *   `gram`, then the update pass, on `stream`; state and outputs as in
+ *   edit_outer_step_layer.  theta and the replicas must be unchanged since
+ *   the Gram was taken.
+ * Checks as in edit_outer_step_layer (gram_layer needs no momentum), plus
+ * `gram` non-NULL, 8-byte aligned and disjoint from the other buffers. */
+edit_status_t edit_outer_gram_layer(edit_outer_t h, int32_t layer, const float *theta,
+                                    void *const *replicas, double *gram, void *stream);
+edit_status_t edit_outer_apply_layer(edit_outer_t h, int32_t layer, const double *gram,
+                                     float *theta, float *momentum, void *const *replicas,
+                                     void *stream);
+
 /* Copy unit `layer`'s EMA state and last decision to *out, after waiting for
  * that unit's last enqueued step.  EDIT_ESTATE if the unit never stepped and
  * no state was set. */

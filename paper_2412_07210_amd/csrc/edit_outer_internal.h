@@ -50,6 +50,12 @@ hipError_t launch_pass1(int K, bool bf16, int rows, const float* theta,
                         const DecideParams& prm, hipStream_t stream);
 hipError_t launch_decide(int K, const double* partials, int rows, UnitRecord* rec,
                          const DecideParams& prm, hipStream_t stream);
+// The fixed-order sum of the partials as a K(K+1)/2 vector in device memory.
+hipError_t launch_gram_reduce(int K, const double* partials, int rows, double* gram,
+                              hipStream_t stream);
+// The decision from a device-resident Gram vector.
+hipError_t launch_decide_gram(int K, const double* gram, UnitRecord* rec, const DecideParams& prm,
+                              hipStream_t stream);
 hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom,
                         void* const* reps, const UnitRecord* rec, int64_t n, double lr,
                         double rho, hipStream_t stream);

@@ -578,6 +578,31 @@ __global__ __launch_bounds__(kDecideThreads) void decide_kernel(const double* __
   if (threadIdx.x < 64) decide<K>(gram, rec, prm);
 }
 
+// The Gram of one unit as a plain vector (upper triangle, row by row): the
+// decision kernel's own fixed-order reduction, written out instead of
+// decided on, so that the shards of one module can add their Grams before a
+// shared decision.
+template <int K>
+__global__ __launch_bounds__(kDecideThreads) void gram_reduce_kernel(const double* __restrict__ partials,
+                                                                     int rows,
+                                                                     double* __restrict__ gram_out) {
+  __shared__ double gram[K * (K + 1) / 2];
+  reduce_partials<K, kDecideThreads, 4>(partials, rows, gram);
+  __syncthreads();
+  for (int p = threadIdx.x; p < K * (K + 1) / 2; p += kDecideThreads) gram_out[p] = gram[p];
+}
+
+// The decision from a Gram supplied by the caller (one wave).
+template <int K>
+__global__ __launch_bounds__(64) void decide_gram_kernel(const double* __restrict__ gram_in,
+                                                         UnitRecord* __restrict__ rec,
+                                                         DecideParams prm) {
+  __shared__ double gram[K * (K + 1) / 2];
+  for (int p = threadIdx.x; p < K * (K + 1) / 2; p += 64) gram[p] = gram_in[p];
+  __syncthreads();
+  decide<K>(gram, rec, prm);
+}
+
 // ---------------------------------------------------------------- pass 2
 
 // theta' and b' of one element, in fp64 from fp32 inputs (rounded once on store):
@@ -770,6 +795,20 @@ hipError_t decide_launch(const double* partials, int rows, UnitRecord* rec, cons
   return hipGetLastError();
 }
 
+template <int K>
+hipError_t gram_reduce_launch(const double* partials, int rows, double* gram, hipStream_t stream) {
+  hipLaunchKernelGGL((gram_reduce_kernel<K>), dim3(1), dim3(kDecideThreads), 0, stream, partials, rows,
+                     gram);
+  return hipGetLastError();
+}
+
+template <int K>
+hipError_t decide_gram_launch(const double* gram, UnitRecord* rec, const DecideParams& prm,
+                              hipStream_t stream) {
+  hipLaunchKernelGGL((decide_gram_kernel<K>), dim3(1), dim3(64), 0, stream, gram, rec, prm);
+  return hipGetLastError();
+}
+
 template <int K, bool BF16>
 hipError_t pass2_launch(int blocks, float* theta, float* mom, void* const* reps,
                         const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
@@ -818,6 +857,32 @@ hipError_t launch_decide(int K, const double* partials, int rows, UnitRecord* re
 #define EDIT_CASE(KK) \
   case KK:            \
     return decide_launch<KK>(partials, rows, rec, prm, stream);
+    EDIT_FOR_EACH_K(EDIT_CASE)
+#undef EDIT_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gram_reduce(int K, const double* partials, int rows, double* gram,
+                              hipStream_t stream) {
+  switch (K) {
+#define EDIT_CASE(KK) \
+  case KK:            \
+    return gram_reduce_launch<KK>(partials, rows, gram, stream);
+    EDIT_FOR_EACH_K(EDIT_CASE)
+#undef EDIT_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_decide_gram(int K, const double* gram, UnitRecord* rec, const DecideParams& prm,
+                              hipStream_t stream) {
+  switch (K) {
+#define EDIT_CASE(KK) \
+  case KK:            \
+    return decide_gram_launch<KK>(gram, rec, prm, stream);
     EDIT_FOR_EACH_K(EDIT_CASE)
 #undef EDIT_CASE
     default:

@@ -199,9 +199,14 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
 
 namespace {
 
-// Argument checks shared by step_layer and step_round.
+// Argument checks shared by the step entry points.  `momentum` may be NULL
+// only when `need_momentum` is false (the Gram pass does not touch it).
+// `extra`, when not NULL, is one more buffer of `extra_bytes` (a Gram vector)
+// that must not overlap the others.
 edit_status_t check_step(const edit_outer* h, int32_t layer, const float* theta,
-                         const float* momentum, void* const* replicas) {
+                         const float* momentum, void* const* replicas,
+                         bool need_momentum = true, const void* extra = nullptr,
+                         int64_t extra_bytes = 0) {
   if (layer < 0 || layer >= h->cfg.num_layers)
     return fail(EDIT_EINVAL, "layer " + std::to_string(layer) + " out of range");
   const Unit& u = h->units[layer];
@@ -209,28 +214,41 @@ edit_status_t check_step(const edit_outer* h, int32_t layer, const float* theta,
   const int64_t n = u.n;
   if (n == 0) return EDIT_OK;
   if (!replicas) return fail(EDIT_EINVAL, "replicas must not be NULL");
-  if (!theta || !momentum) return fail(EDIT_EINVAL, "theta and momentum must not be NULL");
-  if (!aligned16(theta) || !aligned16(momentum))
+  if (!theta || (need_momentum && !momentum))
+    return fail(EDIT_EINVAL, "theta and momentum must not be NULL");
+  if (!aligned16(theta) || (momentum && !aligned16(momentum)))
     return fail(EDIT_EINVAL, "theta and momentum must be 16-byte aligned");
   // Every buffer's byte range, for the alias check.
   struct Range {
     uintptr_t lo, hi;
   };
-  Range r[EDIT_MAX_K + 2];
-  r[0] = {reinterpret_cast<uintptr_t>(theta), reinterpret_cast<uintptr_t>(theta) + 4 * n};
-  r[1] = {reinterpret_cast<uintptr_t>(momentum), reinterpret_cast<uintptr_t>(momentum) + 4 * n};
+  Range r[EDIT_MAX_K + 3];
+  int nr = 0;
+  r[nr++] = {reinterpret_cast<uintptr_t>(theta), reinterpret_cast<uintptr_t>(theta) + 4 * n};
+  if (momentum)
+    r[nr++] = {reinterpret_cast<uintptr_t>(momentum), reinterpret_cast<uintptr_t>(momentum) + 4 * n};
+  if (extra)
+    r[nr++] = {reinterpret_cast<uintptr_t>(extra), reinterpret_cast<uintptr_t>(extra) + extra_bytes};
   const int64_t rb = h->cfg.replica_dtype == EDIT_BF16 ? 2 : 4;
   for (int j = 0; j < K; ++j) {
     if (!replicas[j]) return fail(EDIT_EINVAL, "replica pointer " + std::to_string(j) + " is NULL");
     if (!aligned16(replicas[j]))
       return fail(EDIT_EINVAL, "replica " + std::to_string(j) + " is not 16-byte aligned");
     const uintptr_t p = reinterpret_cast<uintptr_t>(replicas[j]);
-    r[2 + j] = {p, p + rb * n};
+    r[nr++] = {p, p + rb * n};
   }
-  for (int a = 0; a < K + 2; ++a)
-    for (int b = a + 1; b < K + 2; ++b)
+  for (int a = 0; a < nr; ++a)
+    for (int b = a + 1; b < nr; ++b)
       if (r[a].lo < r[b].hi && r[b].lo < r[a].hi)
-        return fail(EDIT_EINVAL, "theta, momentum and the replicas must not overlap");
+        return fail(EDIT_EINVAL, extra ? "theta, momentum, the replicas and gram must not overlap"
+                                       : "theta, momentum and the replicas must not overlap");
+  return EDIT_OK;
+}
+
+// A Gram vector argument: non-NULL and 8-byte aligned.
+edit_status_t check_gram(const void* gram) {
+  if (!gram) return fail(EDIT_EINVAL, "gram must not be NULL");
+  if (reinterpret_cast<uintptr_t>(gram) & 7u) return fail(EDIT_EINVAL, "gram must be 8-byte aligned");
   return EDIT_OK;
 }
 
@@ -280,6 +298,16 @@ struct Enqueue {
                                 prev ? prev->rec : nullptr, prm, s);
     return e == hipSuccess ? EDIT_OK : fail_hip(e, "pass1 launch");
   }
+  edit_status_t gram_out(int32_t layer, double* gram) {
+    Unit& u = h->units[layer];
+    hipError_t e = launch_gram_reduce(K, u.partials, u.rows, gram, s);
+    return e == hipSuccess ? EDIT_OK : fail_hip(e, "gram reduce launch");
+  }
+  edit_status_t decide_from(int32_t layer, const double* gram) {
+    Unit& u = h->units[layer];
+    hipError_t e = launch_decide_gram(K, gram, u.rec, prm, s);
+    return e == hipSuccess ? EDIT_OK : fail_hip(e, "decide launch");
+  }
   edit_status_t decide(int32_t layer) {
     Unit& u = h->units[layer];
     hipError_t e = launch_decide(K, u.partials, u.rows, u.rec, prm, s);
@@ -328,6 +356,41 @@ edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta,
   EDIT_TRY(q.event(h->units[layer], layer, 2));
   EDIT_TRY(q.pass2(layer, theta, momentum, replicas));
   EDIT_TRY(q.event(h->units[layer], layer, 3));
+  return q.finish(layer);
+}
+
+edit_status_t edit_outer_gram_layer(edit_outer_t h, int32_t layer, const float* theta,
+                                    void* const* replicas, double* gram, void* stream) {
+  if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  EDIT_TRY(check_gram(gram));
+  const int K = h->cfg.num_workers;
+  EDIT_TRY(check_step(h, layer, theta, nullptr, replicas, false, gram,
+                      static_cast<int64_t>(num_pairs(K)) * 8));
+  EDIT_TRY(check_device(h));
+  Enqueue q{h, reinterpret_cast<hipStream_t>(stream), decide_params(h), K,
+            h->cfg.replica_dtype == EDIT_BF16};
+  EDIT_TRY(q.pass1(layer, theta, replicas, nullptr));
+  return q.gram_out(layer, gram);
+}
+
+edit_status_t edit_outer_apply_layer(edit_outer_t h, int32_t layer, const double* gram,
+                                     float* theta, float* momentum, void* const* replicas,
+                                     void* stream) {
+  if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  EDIT_TRY(check_gram(gram));
+  const int K = h->cfg.num_workers;
+  EDIT_TRY(check_step(h, layer, theta, momentum, replicas, true, gram,
+                      static_cast<int64_t>(num_pairs(K)) * 8));
+  EDIT_TRY(check_device(h));
+  Enqueue q{h, reinterpret_cast<hipStream_t>(stream), decide_params(h), K,
+            h->cfg.replica_dtype == EDIT_BF16};
+  Unit& u = h->units[layer];
+  EDIT_TRY(q.event(u, layer, 0));
+  EDIT_TRY(q.decide_from(layer, gram));
+  EDIT_TRY(q.event(u, layer, 1));
+  EDIT_TRY(q.event(u, layer, 2));
+  EDIT_TRY(q.pass2(layer, theta, momentum, replicas));
+  EDIT_TRY(q.event(u, layer, 3));
   return q.finish(layer);
 }
 

@@ -28,6 +28,7 @@ EDIT_OK, EDIT_EINVAL, EDIT_ENOMEM, EDIT_EHIP, EDIT_ESTATE, EDIT_ENODEV = 0, -1, 
 # Every function the header declares; the CPU tests check the library exports them.
 EXPORTS = (
     "edit_outer_init", "edit_outer_step_layer", "edit_outer_step_round",
+    "edit_outer_gram_layer", "edit_outer_apply_layer",
     "edit_outer_state_get", "edit_outer_state_set",
     "edit_outer_destroy", "edit_outer_strerror", "edit_outer_last_error",
     "edit_outer_set_profiling", "edit_outer_kernel_times", "edit_outer_copy_probe",
@@ -96,6 +97,10 @@ def load_library() -> ctypes.CDLL:
                                           ctypes.POINTER(vp), ctypes.POINTER(vp),
                                           ctypes.POINTER(vp), vp]
     lib.edit_outer_step_round.restype = st
+    lib.edit_outer_gram_layer.argtypes = [vp, ctypes.c_int32, vp, ctypes.POINTER(vp), vp, vp]
+    lib.edit_outer_gram_layer.restype = st
+    lib.edit_outer_apply_layer.argtypes = [vp, ctypes.c_int32, vp, vp, vp, ctypes.POINTER(vp), vp]
+    lib.edit_outer_apply_layer.restype = st
     lib.edit_outer_state_get.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(_LayerState)]
     lib.edit_outer_state_get.restype = st
     lib.edit_outer_state_set.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(_LayerState)]
@@ -246,6 +251,59 @@ class EditOuter:
                                                      momentum.data_ptr(), ptrs,
                                                      _stream_handle(stream, self.device))
         _check(status, "edit_outer_step_layer")
+
+    @property
+    def num_pairs(self) -> int:
+        """Length of a Gram vector: K(K+1)/2."""
+        K = self.cfg.num_workers
+        return K * (K + 1) // 2
+
+    def _call(self, fn, *args) -> int:
+        if torch.cuda.current_device() != self.device.index:
+            with torch.cuda.device(self.device):
+                return fn(self._h, *args)
+        return fn(self._h, *args)
+
+    def _unit_tensors(self, layer: int, theta, momentum, replicas):
+        if not 0 <= layer < len(self._numel):
+            raise IndexError(f"layer {layer} out of range")
+        n = self._numel[layer]
+        K = self.cfg.num_workers
+        if len(replicas) != K:
+            raise ValueError(f"expected {K} replicas, got {len(replicas)}")
+        self._check_tensor(theta, n, torch.float32, "theta")
+        if momentum is not None:
+            self._check_tensor(momentum, n, torch.float32, "momentum")
+        for j, r in enumerate(replicas):
+            self._check_tensor(r, n, self.cfg.torch_dtype, f"replicas[{j}]")
+        return (ctypes.c_void_p * K)(*[r.data_ptr() for r in replicas])
+
+    def gram_layer(self, layer: int, theta: torch.Tensor, replicas: Sequence[torch.Tensor],
+                   gram: Optional[torch.Tensor] = None,
+                   stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        """Enqueue pass 1 of unit `layer` and return its Gram vector (fp64,
+        K(K+1)/2 upper-triangle sums, row by row) on the device.  For a module
+        sharded over several units, add the shards' vectors and hand the sum
+        to apply_layer of every shard."""
+        ptrs = self._unit_tensors(layer, theta, None, replicas)
+        if gram is None:
+            gram = torch.empty(self.num_pairs, dtype=torch.float64, device=self.device)
+        self._check_tensor(gram, self.num_pairs, torch.float64, "gram")
+        _check(self._call(self._lib.edit_outer_gram_layer, int(layer), theta.data_ptr(), ptrs,
+                          gram.data_ptr(), _stream_handle(stream, self.device)),
+               "edit_outer_gram_layer")
+        return gram
+
+    def apply_layer(self, layer: int, gram: torch.Tensor, theta: torch.Tensor,
+                    momentum: torch.Tensor, replicas: Sequence[torch.Tensor],
+                    stream: Optional[torch.cuda.Stream] = None) -> None:
+        """Enqueue the decision from `gram` and the update pass of unit `layer`."""
+        ptrs = self._unit_tensors(layer, theta, momentum, replicas)
+        self._check_tensor(gram, self.num_pairs, torch.float64, "gram")
+        _check(self._call(self._lib.edit_outer_apply_layer, int(layer), gram.data_ptr(),
+                          theta.data_ptr(), momentum.data_ptr(), ptrs,
+                          _stream_handle(stream, self.device)),
+               "edit_outer_apply_layer")
 
     def prepare_round(self, units: Sequence[tuple],
                       layers: Optional[Sequence[int]] = None) -> "RoundPlan":
