@@ -309,6 +309,9 @@ def main(argv=None) -> int:
     ap.add_argument("--per-unit", action="store_true",
                     help="one edit_outer_step_layer call per unit instead of edit_outer_step_round")
     ap.add_argument("--units", type=int, default=0, help="use only the first N units (0 = all)")
+    ap.add_argument("--shards", type=int, default=1,
+                    help="split every unit into S shards that share one decision through "
+                         "edit_outer_gram_layer / edit_outer_apply_layer (the module-norm path)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--profile-every", type=int, default=6,
                     help="record per-kernel HIP events on every k-th unit (0: none, roofline then null)")
@@ -351,7 +354,19 @@ def main(argv=None) -> int:
     K, R = wl.num_workers, wl.replica_bytes
     hyper = wl.hyper()
     warm_rounds = hyper.pop("warmup_rounds")
-    lib = EditOuter(OuterConfig(num_workers=K, layer_numel=wl.layer_numel, replica_dtype=wl.replica_dtype,
+    S = max(1, args.shards)
+    if S > 1 and (args.per_unit or args.streams > 1):
+        print(json.dumps({"error": "--shards runs its own issue order; drop --per-unit/--streams"}))
+        return 2
+
+    def shard_cuts(n):
+        # contiguous shards whose starts are multiples of 8 elements (16-byte aligned views)
+        step = -(-n // (8 * S)) * 8
+        return [min(n, i * step) for i in range(S)] + [n]
+
+    handle_numel = wl.layer_numel if S == 1 else \
+        [b - a for n in wl.layer_numel for a, b in zip(shard_cuts(n)[:-1], shard_cuts(n)[1:])]
+    lib = EditOuter(OuterConfig(num_workers=K, layer_numel=handle_numel, replica_dtype=wl.replica_dtype,
                                 ema_warmup_rounds=warm_rounds, **hyper), dev)
     log(f"workload {wl.name}: {wl.num_units} units, {wl.total_numel:,} params, K={K}, {wl.replica_dtype}")
 
@@ -362,9 +377,25 @@ def main(argv=None) -> int:
         units.append((th, torch.zeros_like(th), reps))
     torch.cuda.synchronize()
     streams = [torch.cuda.Stream(device=dev) for _ in range(args.streams)] if args.streams > 1 else None
-    plan = lib.prepare_round(units)  # tensors validated once; each step is one C call
-    events = args.profile_every > 0
-    lib.set_profiling(args.profile_every)
+    plan = lib.prepare_round(units) if S == 1 else None  # validated once; each step is one C call
+    shard_views = []  # per unit: [(handle layer, theta, momentum, replicas)] and its Gram buffers
+    for u, (th, b, reps) in enumerate(units):
+        cuts = shard_cuts(th.numel())
+        views = [(u * S + s, th[a:z], b[a:z], [r[a:z] for r in reps])
+                 for s, (a, z) in enumerate(zip(cuts[:-1], cuts[1:]))] if S > 1 else []
+        shard_views.append((views, torch.empty(S, lib.num_pairs, dtype=torch.float64, device=dev),
+                            torch.empty(lib.num_pairs, dtype=torch.float64, device=dev)))
+
+    def sharded_round():
+        for views, grams, total in shard_views:
+            for s, (layer, th, b, reps) in enumerate(views):
+                lib.gram_layer(layer, th, reps, gram=grams[s])
+            torch.sum(grams, dim=0, out=total)  # stands in for the shard group's all-reduce
+            for layer, th, b, reps in views:
+                lib.apply_layer(layer, total, th, b, reps)
+
+    events = args.profile_every > 0 and S == 1
+    lib.set_profiling(args.profile_every if events else 0)
 
     # Input generation leaves dirty lines of the freshly written replicas in
     # L2 and the 256 MB Infinity Cache.  Streaming 1 GiB through the copy
@@ -400,7 +431,9 @@ def main(argv=None) -> int:
         a = torch.cuda.Event(enable_timing=True)
         z = torch.cuda.Event(enable_timing=True)
         a.record()
-        if args.per_unit and streams is None:
+        if S > 1:
+            sharded_round()
+        elif args.per_unit and streams is None:
             for u, (th, b, reps) in enumerate(units):
                 lib.step_layer(u, th, b, reps)
         elif streams is None:
@@ -413,7 +446,7 @@ def main(argv=None) -> int:
             continue
         step_ms.append(a.elapsed_time(z))
         for u, (th, b, reps) in enumerate(units):
-            st = lib.state_get(u)
+            st = lib.state_get(u * S)  # every shard of a module holds the same decision
             active = int(np.count_nonzero(st.weight > 0)) if st.clip_coef > 0 else 0
             b1, b2 = unit_bytes(th.numel(), K, R, active, st.rolled_back)
             p1_bytes += b1
@@ -462,8 +495,10 @@ def main(argv=None) -> int:
             "replica_dtype": wl.replica_dtype,
             "master_dtype": "f32",
             "streams": args.streams,
-            "entry_point": "edit_outer_step_layer per unit" if args.per_unit else
-                           ("edit_outer_step_round" if args.streams <= 1 else "edit_outer_step_layer, streams"),
+            "entry_point": ("edit_outer_gram_layer + sum + edit_outer_apply_layer per shard" if S > 1 else
+                            "edit_outer_step_layer per unit" if args.per_unit else
+                            "edit_outer_step_round" if args.streams <= 1 else "edit_outer_step_layer, streams"),
+            "shards_per_unit": S,
             "cache_settle_before_step": not args.no_settle,
             "parallelism": "single GPU, K replicas reduced in HBM",
         },

@@ -50,6 +50,19 @@ extern "C" {
 #define EDIT_WA 2u /* norm-based weighted averaging (Eq. 2)        */
 #define EDIT_GC 4u /* pseudo-gradient clip (Eq. 4-5)               */
 
+/* One-pass mean step, allowed only with AE, WA and GC all clear (the
+ * "w/o ALL" ablation of Sec. 4.5, i.e. the DiLoCo outer step): the weights
+ * are then 1/K whatever the norms are, so the average, Nesterov and the
+ * write-back run in a single pass over theta, b and the replicas (48 bytes
+ * per element at K = 8, bf16, against 68 for the two-pass step).  The norms
+ * G_j and ||Delta_bar|| are still computed on the way and reported by
+ * edit_outer_state_get.  Unlike the two-pass step, a worker with a
+ * non-finite norm is NOT left out (there is no norm before the average): its
+ * NaN/Inf reaches theta and shows in its reported G_j.  The Gram entry
+ * points (edit_outer_gram_layer / _apply_layer) are not available in this
+ * mode. */
+#define EDIT_ONE_PASS 8u
+
 typedef struct edit_outer *edit_outer_t; /* opaque, library-owned */
 
 typedef enum {
@@ -68,7 +81,7 @@ typedef struct {
   int32_t num_layers;         /* L sync units (modules), >= 1                  */
   const int64_t *layer_numel; /* [L] elements per unit (>= 0); copied at init  */
   int32_t replica_dtype;      /* edit_dtype_t of the K replicas                */
-  uint32_t flags;             /* EDIT_AE | EDIT_WA | EDIT_GC                   */
+  uint32_t flags;             /* EDIT_AE | EDIT_WA | EDIT_GC, or EDIT_ONE_PASS */
   double outer_lr;            /* nu  (paper: 0.8 or 1.0)                       */
   double momentum;            /* rho (paper: 0.85 or 0.8)                      */
   double clip_threshold;      /* phi of Eq. 4 (paper: 10)                      */
@@ -154,7 +167,8 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
  *   edit_outer_step_layer.  theta and the replicas must be unchanged since
  *   the Gram was taken.
  * Checks as in edit_outer_step_layer (gram_layer needs no momentum), plus
- * `gram` non-NULL, 8-byte aligned and disjoint from the other buffers. */
+ * `gram` non-NULL, 8-byte aligned and disjoint from the other buffers;
+ * EDIT_EINVAL on a handle made with EDIT_ONE_PASS. */
 edit_status_t edit_outer_gram_layer(edit_outer_t h, int32_t layer, const float *theta,
                                     void *const *replicas, double *gram, void *stream);
 edit_status_t edit_outer_apply_layer(edit_outer_t h, int32_t layer, const double *gram,
@@ -189,7 +203,10 @@ edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t every);
 
 /* Durations in ms of the last profiled step of `layer`: ms[0] its norm/Gram
  * pass plus its decision kernel (in a round: its norm/Gram launch, which also
- * carries the previous unit's decision), ms[1] its update pass.  Waits for it. */
+ * carries the previous unit's decision), ms[1] its update pass.  With
+ * EDIT_ONE_PASS: ms[0] the fused pass, ms[1] the record reduction when the
+ * unit was stepped alone (0 in a round, which reduces all units in one launch
+ * at its end).  Waits for it. */
 edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[2]);
 
 /* Plain device-to-device copy kernel of nbytes (a multiple of 16, 16-byte

@@ -11,6 +11,7 @@ namespace edit {
 
 constexpr int kThreads = 256;        // threads per block of the Gram pass
 constexpr int kPass2Threads = 128;   // threads per block of the update pass
+constexpr int kFusedThreads = 128;   // threads per block of the one-pass mean step
 constexpr int kMaxK = EDIT_MAX_K;
 constexpr int kMaxPairs = kMaxK * (kMaxK + 1) / 2;
 
@@ -30,7 +31,16 @@ struct alignas(16) UnitRecord {
   int32_t use_deltas;       // 0: no worker has a non-zero coefficient
   int32_t z_tested;
   int32_t stepped;          // at least one step or state_set happened
+  int32_t finish_pending;   // one-pass mode: partials written, record not yet made
   uint8_t anomalous[kMaxK];
+};
+
+// Where the one-pass record reduction of a unit finds its inputs.
+struct FinishEntry {
+  const double* partials;
+  UnitRecord* rec;
+  int32_t rows;
+  int32_t pad;
 };
 
 struct DecideParams {
@@ -59,6 +69,15 @@ hipError_t launch_decide_gram(int K, const double* gram, UnitRecord* rec, const 
 hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom,
                         void* const* reps, const UnitRecord* rec, int64_t n, double lr,
                         double rho, hipStream_t stream);
+// One-pass mean step (no penalty components): `rows` blocks of
+// fused_vectors_per_thread(bf16) * kFusedThreads vectors each, leaving
+// (K+1) x rows norm partials and the unit marked; then one block per entry
+// of `table` turns marked units' partials into their records.
+int fused_vectors_per_thread(bool bf16);
+hipError_t launch_fused_mean(int K, bool bf16, int rows, float* theta, float* mom,
+                             void* const* reps, double* partials, UnitRecord* rec, int64_t n,
+                             double lr, double rho, hipStream_t stream);
+hipError_t launch_fused_finish(int K, const FinishEntry* table, int units, hipStream_t stream);
 hipError_t launch_copy(void* dst, const void* src, int64_t nbytes, int blocks,
                        hipStream_t stream);
 

@@ -733,6 +733,171 @@ __global__ __launch_bounds__(kPass2Threads) void pass2_update_kernel(float* __re
   }
 }
 
+// ------------------------------------------------------ one-pass mean step
+
+// With every penalty component off (the plain DiLoCo outer step, the paper's
+// "w/o ALL" ablation), the weights are 1/K whatever the norms are, so the
+// average, Nesterov and the write-back need no earlier pass: one kernel reads
+// theta, b and the K replicas once and writes theta', b' and the replicas.
+// The norms G_j and ||Delta_bar|| are still summed on the way (per-block
+// partials, reduced by fused_finish_kernel) for the step's record, and the
+// unit is marked for that reduction.  A block owns V*kFusedThreads
+// consecutive vectors; a thread loads its V vectors of every buffer before
+// computing, so V*(K+2) 16-byte loads are in flight per thread (V = 2 for
+// bf16 replicas measured best here: one vector leaves the block's closing
+// reduction exposed, four cost occupancy).
+template <int K, bool BF16, bool NT, int V>
+__global__ __launch_bounds__(kFusedThreads) void fused_mean_kernel(float* __restrict__ theta,
+                                                                   float* __restrict__ mom,
+                                                                   MutPtrs<K> reps,
+                                                                   double* __restrict__ partials,
+                                                                   UnitRecord* __restrict__ rec,
+                                                                   int64_t nvec, int64_t n,
+                                                                   double lr, double rho) {
+  constexpr int VE = Vec<BF16>::VE;
+  constexpr double inv_k = 1.0 / K;
+  const int rows = gridDim.x;
+  const int b = blockIdx.x;
+  double sq[K + 1];  // sum of Delta_j^2 per worker, then of Delta_bar^2
+#pragma unroll
+  for (int p = 0; p <= K; ++p) sq[p] = 0.0;
+
+  {
+    const int64_t base = static_cast<int64_t>(b) * V * kFusedThreads + threadIdx.x;
+    float th[V][VE], bm[V][VE];
+    u32x4 raw[V][K];
+#pragma unroll
+    for (int u = 0; u < V; ++u) {
+      const int64_t v = base + u * kFusedThreads;
+      if (v < nvec) {
+        load_f32<VE, NT>(theta, v, th[u]);
+        load_f32<VE, NT>(mom, v, bm[u]);
+#pragma unroll
+        for (int j = 0; j < K; ++j) raw[u][j] = ld16<NT>(reinterpret_cast<const u32x4*>(reps.p[j]) + v);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < V; ++u) {
+      const int64_t v = base + u * kFusedThreads;
+      if (v < nvec) {
+        float tn[VE], bn[VE];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          double sum = 0.0;
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            const double d = delta64<BF16>(raw[u][j], e, th[u][e]);
+            sq[j] = fma(d, d, sq[j]);
+            sum += d;
+          }
+          const double dbar = sum * inv_k;  // Eq. 3 with w_j = 1/K
+          sq[K] = fma(dbar, dbar, sq[K]);
+          nesterov(dbar, th[u][e], bm[u][e], lr, rho, tn[e], bn[e]);
+        }
+        store_f32<VE, NT>(theta, v, tn);
+        store_f32<VE, NT>(mom, v, bn);
+        const u32x4 out = pack<BF16>(tn);
+#pragma unroll
+        for (int j = 0; j < K; ++j) st16<NT>(reinterpret_cast<u32x4*>(reps.p[j]) + v, out);
+      }
+    }
+  }
+  const int64_t tail = nvec * VE + threadIdx.x;  // the last n - nvec*VE elements
+  if (b == 0 && tail < n) {
+    const float t0 = theta[tail];
+    double sum = 0.0;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      const double d = static_cast<double>(load_scalar<BF16>(reps.p[j], tail)) - static_cast<double>(t0);
+      sq[j] = fma(d, d, sq[j]);
+      sum += d;
+    }
+    const double dbar = sum * inv_k;
+    sq[K] = fma(dbar, dbar, sq[K]);
+    float tn, bn;
+    nesterov(dbar, t0, mom[tail], lr, rho, tn, bn);
+    theta[tail] = tn;
+    mom[tail] = bn;
+#pragma unroll
+    for (int j = 0; j < K; ++j) store_scalar<BF16>(reps.p[j], tail, tn);
+  }
+
+  // block sums in a fixed order: wave butterfly, then the waves in order
+  constexpr int kWaves = kFusedThreads / 64;
+  __shared__ double red[kWaves][K + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int p = 0; p <= K; ++p) {
+    const double t = wave_sum(sq[p]);
+    if (lane == 0) red[wave][p] = t;
+  }
+  __syncthreads();
+  if (threadIdx.x <= K) {
+    double t = red[0][threadIdx.x];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) t += red[w][threadIdx.x];
+    partials[static_cast<int64_t>(threadIdx.x) * rows + b] = t;
+  }
+  if (b == 0 && threadIdx.x == 0) rec->finish_pending = 1;
+}
+
+// The records of one-pass steps: G_j and ||Delta_bar|| from each unit's
+// partials (in a fixed order), w_j = 1/K, beta = 1.  One block per unit of
+// `table`; units whose fused pass has not run since their last record are
+// skipped, so a round can take all its units' reductions in one launch after
+// its last fused pass.  Nothing is masked in this mode: a non-finite replica
+// shows up as a non-finite G_j (and in theta).
+template <int K>
+__global__ __launch_bounds__(kDecideThreads) void fused_finish_kernel(const FinishEntry* __restrict__ table) {
+  const FinishEntry ent = table[blockIdx.x];
+  UnitRecord* rec = ent.rec;
+  if (!rec->finish_pending) return;  // block-uniform
+  const double* partials = ent.partials;
+  const int rows = ent.rows;
+  constexpr int NV = K + 1;
+  constexpr int kWaves = kDecideThreads / 64;
+  __shared__ double red[kWaves][NV];
+  __shared__ double tot[NV];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  double s[NV];
+#pragma unroll
+  for (int q = 0; q < NV; ++q) s[q] = 0.0;
+#pragma unroll 4
+  for (int r = threadIdx.x; r < rows; r += kDecideThreads)
+#pragma unroll
+    for (int q = 0; q < NV; ++q) s[q] += partials[static_cast<int64_t>(q) * rows + r];
+#pragma unroll
+  for (int q = 0; q < NV; ++q) {
+    const double t = wave_sum(s[q]);
+    if (lane == 0) red[wave][q] = t;
+  }
+  __syncthreads();
+  if (threadIdx.x < NV) {
+    double t = red[0][threadIdx.x];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) t += red[w][threadIdx.x];
+    tot[threadIdx.x] = t;
+  }
+  __syncthreads();
+  if (threadIdx.x < K) {
+    rec->norm[threadIdx.x] = sqrt(tot[threadIdx.x]);
+    rec->weight[threadIdx.x] = 1.0 / K;
+    rec->coef[threadIdx.x] = 1.0 / K;
+    rec->src[threadIdx.x] = threadIdx.x;
+    rec->anomalous[threadIdx.x] = 0;
+  }
+  if (threadIdx.x == 0) {
+    rec->synced_norm = sqrt(tot[K]);
+    rec->clip_coef = 1.0;
+    rec->use_deltas = 1;
+    rec->rollback = 0;
+    rec->z_tested = 0;
+    rec->stepped = 1;
+    rec->round = rec->round + 1;
+    rec->finish_pending = 0;
+  }
+}
+
 // ------------------------------------------------------------ copy probe
 
 template <int U, bool NT>
@@ -820,6 +985,30 @@ hipError_t pass2_launch(int blocks, float* theta, float* mom, void* const* reps,
   return hipGetLastError();
 }
 
+// Vectors per thread of the one-pass kernel (measured: two 16-byte vectors
+// of bf16 replicas, one of fp32).
+template <bool BF16>
+constexpr int fused_v() {
+  return BF16 ? 2 : 1;
+}
+
+template <int K, bool BF16>
+hipError_t fused_mean_launch(int rows, float* theta, float* mom, void* const* reps, double* partials,
+                             UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
+  MutPtrs<K> rp;
+  for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
+  const int64_t nvec = n / Vec<BF16>::VE;
+  hipLaunchKernelGGL((fused_mean_kernel<K, BF16, kNT2, fused_v<BF16>()>), dim3(rows), dim3(kFusedThreads),
+                     0, stream, theta, mom, rp, partials, rec, nvec, n, lr, rho);
+  return hipGetLastError();
+}
+
+template <int K>
+hipError_t fused_finish_launch(const FinishEntry* table, int units, hipStream_t stream) {
+  hipLaunchKernelGGL((fused_finish_kernel<K>), dim3(units), dim3(kDecideThreads), 0, stream, table);
+  return hipGetLastError();
+}
+
 template <typename Kern>
 int occupancy(Kern kernel) {
   int blocks = 0;
@@ -897,6 +1086,37 @@ hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom, 
   case KK:                                                                                     \
     return bf16 ? pass2_launch<KK, true>(blocks, theta, mom, reps, rec, n, lr, rho, stream)    \
                 : pass2_launch<KK, false>(blocks, theta, mom, reps, rec, n, lr, rho, stream);
+    EDIT_FOR_EACH_K(EDIT_CASE)
+#undef EDIT_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+int fused_vectors_per_thread(bool bf16) { return bf16 ? fused_v<true>() : fused_v<false>(); }
+
+hipError_t launch_fused_mean(int K, bool bf16, int rows, float* theta, float* mom, void* const* reps,
+                             double* partials, UnitRecord* rec, int64_t n, double lr, double rho,
+                             hipStream_t stream) {
+  switch (K) {
+#define EDIT_CASE(KK)                                                                              \
+  case KK:                                                                                         \
+    return bf16 ? fused_mean_launch<KK, true>(rows, theta, mom, reps, partials, rec, n, lr, rho,   \
+                                              stream)                                              \
+                : fused_mean_launch<KK, false>(rows, theta, mom, reps, partials, rec, n, lr, rho,  \
+                                               stream);
+    EDIT_FOR_EACH_K(EDIT_CASE)
+#undef EDIT_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_fused_finish(int K, const FinishEntry* table, int units, hipStream_t stream) {
+  switch (K) {
+#define EDIT_CASE(KK) \
+  case KK:            \
+    return fused_finish_launch<KK>(table, units, stream);
     EDIT_FOR_EACH_K(EDIT_CASE)
 #undef EDIT_CASE
     default:

@@ -34,7 +34,7 @@ edit_status_t fail_hip(hipError_t e, const char* what) {
 
 struct Unit {
   int64_t n = 0;
-  int rows = 1;         // pass-1 blocks = partial rows
+  int rows = 1;         // pass-1 blocks = partial rows (one-pass mode: fused blocks)
   int blocks2 = 1;      // pass-2 blocks
   double* partials = nullptr;
   UnitRecord* rec = nullptr;
@@ -55,6 +55,8 @@ struct edit_outer {
   int cap1 = 1;            // resident blocks of pass 1 on the whole GPU
   int32_t profile_every = 0;  // record kernel events on units l with l % every == 0
   char* arena = nullptr;   // one device allocation for every unit's scratch
+  FinishEntry* finish_table = nullptr;  // one-pass mode: [L] entries, in the arena
+  bool one_pass = false;
   std::vector<Unit> units;
 };
 
@@ -115,7 +117,10 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
   if (!cfg->layer_numel) return fail(EDIT_EINVAL, "layer_numel must not be NULL");
   if (cfg->replica_dtype != EDIT_F32 && cfg->replica_dtype != EDIT_BF16)
     return fail(EDIT_EINVAL, "replica_dtype must be EDIT_F32 or EDIT_BF16");
-  if (cfg->flags & ~(EDIT_AE | EDIT_WA | EDIT_GC)) return fail(EDIT_EINVAL, "unknown flag bits");
+  if (cfg->flags & ~(EDIT_AE | EDIT_WA | EDIT_GC | EDIT_ONE_PASS))
+    return fail(EDIT_EINVAL, "unknown flag bits");
+  if ((cfg->flags & EDIT_ONE_PASS) && (cfg->flags & (EDIT_AE | EDIT_WA | EDIT_GC)))
+    return fail(EDIT_EINVAL, "flag EDIT_ONE_PASS needs EDIT_AE, EDIT_WA and EDIT_GC clear");
   if (!(cfg->ema_alpha > 0.0 && cfg->ema_alpha <= 1.0))
     return fail(EDIT_EINVAL, "ema_alpha must be in (0, 1]");
   if (!(cfg->clip_eps > 0.0)) return fail(EDIT_EINVAL, "clip_eps must be > 0");
@@ -147,6 +152,7 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
   h->num_cu = prop.multiProcessorCount;
   const bool bf16 = cfg->replica_dtype == EDIT_BF16;
   h->cap1 = h->num_cu * pass1_blocks_per_cu(K, bf16);
+  h->one_pass = (cfg->flags & EDIT_ONE_PASS) != 0;
 
   // Lay out every unit's record and partials in one allocation.
   const int ve = bf16 ? 8 : 4;
@@ -163,16 +169,23 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
     // paths reduce in the same order)
     u.rows = static_cast<int>(
         std::max<int64_t>(1, std::min<int64_t>(h->cap1 - 1, ceil_div(nvec, kThreads))));
-    // pass 2: one vector per thread (block count grows with the unit)
+    // pass 2 (and the one-pass kernel): a fixed number of vectors per thread,
+    // so the block count grows with the unit
     if (ceil_div(nvec, kPass2Threads) > INT32_MAX) {
       delete h;
       return fail(EDIT_EINVAL, "layer_numel[" + std::to_string(l) + "] is too large");
     }
     u.blocks2 = static_cast<int>(std::max<int64_t>(1, ceil_div(nvec, kPass2Threads)));
+    if (h->one_pass)
+      u.rows = static_cast<int>(std::max<int64_t>(
+          1, ceil_div(nvec, int64_t(kFusedThreads) * fused_vectors_per_thread(bf16))));
     offs[l] = total;
-    const size_t part_bytes = (size_t(num_pairs(K)) * u.rows * sizeof(double) + 255) & ~size_t(255);
+    const size_t per_row = h->one_pass ? size_t(K + 1) : size_t(num_pairs(K));
+    const size_t part_bytes = (per_row * u.rows * sizeof(double) + 255) & ~size_t(255);
     total += rec_bytes + part_bytes;
   }
+  const size_t table_off = total;
+  if (h->one_pass) total += (sizeof(FinishEntry) * cfg->num_layers + 255) & ~size_t(255);
   e = hipMalloc(reinterpret_cast<void**>(&h->arena), total);
   if (e != hipSuccess) {
     delete h;
@@ -184,6 +197,14 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
     u.rec = reinterpret_cast<UnitRecord*>(h->arena + offs[l]);
     u.partials = reinterpret_cast<double*>(h->arena + offs[l] + rec_bytes);
     e = hipEventCreateWithFlags(&u.done, hipEventDisableTiming);
+  }
+  if (e == hipSuccess && h->one_pass) {
+    std::vector<FinishEntry> table(cfg->num_layers);
+    for (int l = 0; l < cfg->num_layers; ++l)
+      table[l] = {h->units[l].partials, h->units[l].rec, h->units[l].rows, 0};
+    h->finish_table = reinterpret_cast<FinishEntry*>(h->arena + table_off);
+    e = hipMemcpy(h->finish_table, table.data(), sizeof(FinishEntry) * table.size(),
+                  hipMemcpyHostToDevice);
   }
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
@@ -321,6 +342,19 @@ struct Enqueue {
     if (e != hipSuccess) return fail_hip(e, "pass2 launch");
     return EDIT_OK;
   }
+  // one-pass mode: the fused pass of `layer`, and the record reduction of
+  // `units` table entries from `first` (marked units only)
+  edit_status_t fused(int32_t layer, float* theta, float* momentum, void* const* replicas) {
+    Unit& u = h->units[layer];
+    void* const* mreps = u.n == 0 ? kNoReplicas : replicas;
+    hipError_t e = launch_fused_mean(K, bf16, u.rows, theta, momentum, mreps, u.partials, u.rec, u.n,
+                                     h->cfg.outer_lr, h->cfg.momentum, s);
+    return e == hipSuccess ? EDIT_OK : fail_hip(e, "one-pass launch");
+  }
+  edit_status_t records(int32_t first, int32_t units) {
+    hipError_t e = launch_fused_finish(K, h->finish_table + first, units, s);
+    return e == hipSuccess ? EDIT_OK : fail_hip(e, "record launch");
+  }
   edit_status_t finish(int32_t layer) {
     Unit& u = h->units[layer];
     hipError_t e = hipEventRecord(u.done, s);
@@ -349,6 +383,15 @@ edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta,
   EDIT_TRY(check_device(h));
   Enqueue q{h, reinterpret_cast<hipStream_t>(stream), decide_params(h), h->cfg.num_workers,
             h->cfg.replica_dtype == EDIT_BF16};
+  if (h->one_pass) {
+    EDIT_TRY(q.event(h->units[layer], layer, 0));
+    EDIT_TRY(q.fused(layer, theta, momentum, replicas));
+    EDIT_TRY(q.event(h->units[layer], layer, 1));
+    EDIT_TRY(q.event(h->units[layer], layer, 2));
+    EDIT_TRY(q.records(layer, 1));
+    EDIT_TRY(q.event(h->units[layer], layer, 3));
+    return q.finish(layer);
+  }
   EDIT_TRY(q.event(h->units[layer], layer, 0));
   EDIT_TRY(q.pass1(layer, theta, replicas, nullptr));
   EDIT_TRY(q.decide(layer));
@@ -362,6 +405,7 @@ edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta,
 edit_status_t edit_outer_gram_layer(edit_outer_t h, int32_t layer, const float* theta,
                                     void* const* replicas, double* gram, void* stream) {
   if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  if (h->one_pass) return fail(EDIT_EINVAL, "the Gram entry points are not available with EDIT_ONE_PASS");
   EDIT_TRY(check_gram(gram));
   const int K = h->cfg.num_workers;
   EDIT_TRY(check_step(h, layer, theta, nullptr, replicas, false, gram,
@@ -377,6 +421,7 @@ edit_status_t edit_outer_apply_layer(edit_outer_t h, int32_t layer, const double
                                      float* theta, float* momentum, void* const* replicas,
                                      void* stream) {
   if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  if (h->one_pass) return fail(EDIT_EINVAL, "the Gram entry points are not available with EDIT_ONE_PASS");
   EDIT_TRY(check_gram(gram));
   const int K = h->cfg.num_workers;
   EDIT_TRY(check_step(h, layer, theta, momentum, replicas, true, gram,
@@ -411,6 +456,21 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
   EDIT_TRY(check_device(h));
   Enqueue q{h, reinterpret_cast<hipStream_t>(stream), decide_params(h), K,
             h->cfg.replica_dtype == EDIT_BF16};
+  if (h->one_pass) {
+    // No later kernel of the round needs a unit's record, so the fused passes
+    // run back to back and one launch then reduces every stepped unit's norms.
+    for (int32_t i = 0; i < count; ++i) {
+      const int32_t l = layers[i];
+      EDIT_TRY(q.event(h->units[l], l, 0));
+      EDIT_TRY(q.fused(l, theta[i], momentum[i], replicas + static_cast<size_t>(i) * K));
+      EDIT_TRY(q.event(h->units[l], l, 1));
+      EDIT_TRY(q.event(h->units[l], l, 2));
+      EDIT_TRY(q.event(h->units[l], l, 3));
+    }
+    EDIT_TRY(q.records(0, h->cfg.num_layers));
+    for (int32_t i = 0; i < count; ++i) EDIT_TRY(q.finish(layers[i]));
+    return EDIT_OK;
+  }
   // A large unit runs p1 -> decide -> p2 back to back: its pass 2 walks the
   // unit from the end and finds what pass 1 read last still in the Infinity
   // Cache, which is worth more than the decision's launch.  A small unit's

@@ -21,6 +21,7 @@ LIBRARY = os.path.join(PKG, "libedit_outer.so")
 
 MAX_K = 16
 AE, WA, GC = 1, 2, 4
+ONE_PASS = 8  # single-pass mean step; only with AE, WA and GC clear
 F32, BF16 = 0, 1
 
 EDIT_OK, EDIT_EINVAL, EDIT_ENOMEM, EDIT_EHIP, EDIT_ESTATE, EDIT_ENODEV = 0, -1, -2, -3, -4, -5

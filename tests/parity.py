@@ -156,7 +156,9 @@ class ParityRun:
                                          replica_dtype=wl.replica_dtype,
                                          ema_warmup_rounds=hyper.pop("warmup_rounds"), **hyper, **kw),
                              device=self.device)
-        ocfg = OracleConfig(**wl.hyper(), **kw)
+        # the oracle knows the three penalty components; the library's one-pass
+        # mode (flag 8) is the same method with all three off
+        ocfg = OracleConfig(**wl.hyper(), **({} if flags is None else {"flags": flags & 7}))
         self.cases: List[UnitCase] = []
         for u in units:
             th = wl.init_theta(u, self.device, seed)

@@ -70,7 +70,9 @@ def _init(**over):
     (dict(num_workers=17), "num_workers"),
     (dict(num_layers=0), "num_layers"),
     (dict(replica_dtype=7), "replica_dtype"),
-    (dict(flags=8), "flag"),
+    (dict(flags=16), "flag"),
+    (dict(flags=8 | 1), "EDIT_ONE_PASS"),
+    (dict(flags=8 | 4), "EDIT_ONE_PASS"),
     (dict(ema_alpha=0.0), "ema_alpha"),
     (dict(ema_alpha=1.5), "ema_alpha"),
     (dict(clip_eps=0.0), "clip_eps"),
