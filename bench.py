@@ -9,7 +9,8 @@ cast(theta_t + s_j * N(0, 1e-3)), i.e. what K workers would hold after their
 inner steps; the timed region is the outer step alone, with all inputs
 resident in HBM.
 
-Prints ONE JSON line (see the field notes in the design doc).
+Prints ONE JSON line: the metric, value (GB/s of algorithmic bytes), ms per step,
+the dominant kernel's roofline and the oracle's CPU baseline.
 """
 from __future__ import annotations
 
@@ -41,13 +42,17 @@ def kernel_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def unit_bytes(n: int, K: int, R: int, active: int, rolled_back: bool) -> tuple:
+def unit_bytes(n: int, K: int, R: int, active: int, rolled_back: bool, one_pass: bool = False) -> tuple:
     """Algorithmic HBM bytes of one unit's step: (pass 1, pass 2).
 
     pass 1 reads theta (4 B) and the K replicas; pass 2 reads theta, b and the
     replicas of contributing workers, writes theta, b and all K replicas.  On
-    a rollback pass 2 reads theta and writes the K replicas only.
+    a rollback pass 2 reads theta and writes the K replicas only.  The
+    one-pass mean step reads theta, b and the K replicas and writes them all
+    (reported as its first element, the second being 0).
     """
+    if one_pass:
+        return n * (16 + 2 * K * R), 0
     p1 = n * (4 + K * R)
     if rolled_back:
         p2 = n * (4 + K * R)
@@ -56,9 +61,9 @@ def unit_bytes(n: int, K: int, R: int, active: int, rolled_back: bool) -> tuple:
     return p1, p2
 
 
-def measured_traffic(per_launch_units: float):
-    """HBM bytes per pass-2 launch from committed rocprofv3 counters, if they
-    were taken on the current kernel source; else None."""
+def measured_traffic(kernel: str = "pass2"):
+    """HBM bytes per launch of `kernel` (pass2, fused) from committed rocprofv3
+    counters, if they were taken on the current kernel source; else None."""
     try:
         with open(COUNTERS_FILE) as f:
             data = json.load(f)
@@ -67,7 +72,7 @@ def measured_traffic(per_launch_units: float):
     if data.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
     try:
-        return float(data["pass2_bytes_per_launch"])
+        return float(data[f"{kernel}_bytes_per_launch"])
     except (KeyError, TypeError, ValueError):
         return None
 
@@ -89,20 +94,21 @@ def copy_probe_gbps(torch, outer, nbytes: int = 2 << 30, reps: int = 5) -> float
     return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
-def cpu_baseline(samples, wl, seconds_hint: float):
-    """Time the CPU oracle (one thread, as it stands) on the captured units."""
+def cpu_baseline(samples, wl, seconds_hint: float, one_pass: bool = False):
+    """Time the CPU oracle (one thread, as it stands) on the captured units;
+    for the one-pass mode, the oracle with every penalty component off."""
     import numpy as np
     from oracle import OracleConfig, OracleUnit
 
     K, R = wl.num_workers, wl.replica_bytes
     total_bytes, total_s, done = 0, 0.0, 0
     for (u, theta, mom, reps) in samples:
-        unit = OracleUnit(K, OracleConfig(**wl.hyper()))
+        unit = OracleUnit(K, OracleConfig(**wl.hyper(), **({"flags": 0} if one_pass else {})))
         t0 = time.perf_counter()
         unit.step(theta, mom, reps)
         dt = time.perf_counter() - t0
         total_s += dt
-        total_bytes += theta.size * (3 * K * R + 20)
+        total_bytes += theta.size * ((2 * K * R + 16) if one_pass else (3 * K * R + 20))
         done += 1
         log(f"cpu oracle unit {u}: {dt:.2f} s")
         if total_s > seconds_hint:
@@ -123,19 +129,28 @@ def cpu_baseline(samples, wl, seconds_hint: float):
 # Summaries of rocprofv3 output (CPU only): --summarize-profiles
 # ----------------------------------------------------------------------------
 
-PROFILE_CMDS = {
-    "trace": "rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace -o c3 -- "
-             "python bench.py --steps 20 --warmup 10 --no-cpu-baseline",
-    "fetch": "rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/prof_fetch -o c3 -- "
-             "python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0",
-    "write": "rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/prof_write -o c3 -- "
-             "python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0",
-}
+def _profile_cmds(variant: str) -> dict:
+    """The rocprofv3 commands whose output summarize_profiles reads."""
+    tag, flag = ("c3op", " --one-pass") if variant == "one-pass" else ("c3", "")
+    sfx = "_op" if variant == "one-pass" else ""
+    return {
+        "tag": tag, "suffix": sfx,
+        "trace": f"rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace{sfx} -o {tag} -- "
+                 f"python bench.py --steps 20 --warmup 10 --no-cpu-baseline{flag}",
+        "fetch": f"rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/prof_fetch{sfx} -o {tag} -- "
+                 f"python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0{flag}",
+        "write": f"rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/prof_write{sfx} -o {tag} -- "
+                 f"python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0{flag}",
+    }
+
+
+SHORT = {"pass1_gram_kernel": "pass1", "decide_kernel": "decide", "pass2_update_kernel": "pass2",
+         "fused_mean_kernel": "fused", "fused_finish_kernel": "finish"}
 
 
 def _kernel_kind(name: str) -> str:
     for kind in ("pass1_gram_kernel", "pass1_gram_mfma_kernel", "decide_kernel", "pass2_update_kernel",
-                 "copy_kernel"):
+                 "fused_mean_kernel", "fused_finish_kernel", "copy_kernel"):
         if kind in name:
             return kind
     return ""
@@ -175,7 +190,7 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
     algo = lambda kind, n: {"pass1_gram_kernel": n * (4 + K * R), "pass1_gram_mfma_kernel": n * (4 + K * R),
                             "pass2_update_kernel": n * (16 + 2 * K * R)}.get(kind)
     lines = [f"# Kernel durations by unit size: {wl.description}", "",
-             "Command (from the repository root; `<out>` = gpurun_out):", "",
+             "Command (from the repository root; `<out>` = the directory the profiler wrote to):", "",
              f"    rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace_{name} -o {name} -- "
              f"python bench.py --config {name} --steps 10 --warmup 5 --no-cpu-baseline", "",
              f"Summarised with `python bench.py --summarize-trace <out> {name}` (groups the trace's "
@@ -200,36 +215,44 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
     return text
 
 
-def summarize_profiles(out_dir: str, bench_json: str) -> None:
-    """Turn rocprofv3 CSVs of the 1B K=8 workload into profiles/*.md and the
-    counters file bench.py reads for the roofline's `traffic`."""
+def summarize_profiles(out_dir: str, bench_json: str, variant: str = "two-pass") -> None:
+    """Turn rocprofv3 CSVs of the 1B K=8 workload (two-pass step, or the
+    one-pass mean step) into profiles/*.md and the counters file bench.py
+    reads for the roofline's `traffic`."""
     import csv
     from paper_2412_07210_amd import synth
 
+    cmds = _profile_cmds(variant)
+    tag, sfx = cmds["tag"], cmds["suffix"]
+    one = variant == "one-pass"
+    kinds = ("fused_mean_kernel", "fused_finish_kernel") if one else \
+        ("pass1_gram_kernel", "decide_kernel", "pass2_update_kernel")
+    dominant = "fused_mean_kernel" if one else "pass2_update_kernel"
     wl = synth.get("c3")
     n, K, R = wl.layer_numel[0], wl.num_workers, wl.replica_bytes
     algo = {"pass1_gram_kernel": n * (4 + K * R),
-            "pass2_update_kernel": n * (8 + K * R + 8 + K * R)}
-    algo_rw = {"pass1_gram_kernel": (n * (4 + K * R), 0),
-               "pass2_update_kernel": (n * (8 + K * R), n * (8 + K * R))}
+            "pass2_update_kernel": n * (8 + K * R + 8 + K * R),
+            "fused_mean_kernel": n * (8 + K * R + 8 + K * R)}
+    title = "one-pass mean step (no penalty components)" if one else "outer step"
     prof_dir = os.path.join(ROOT, "profiles")
     os.makedirs(prof_dir, exist_ok=True)
+    name = "c3_one_pass" if one else "c3"
     with open(bench_json) as f:
         bench = json.load(f)
 
     # kernel trace statistics
     stats = {}
-    with open(os.path.join(out_dir, "prof_trace", "c3_kernel_stats.csv")) as f:
+    with open(os.path.join(out_dir, f"prof_trace{sfx}", f"{tag}_kernel_stats.csv")) as f:
         for row in csv.DictReader(f):
             kind = _kernel_kind(row["Name"])
             if kind:
                 stats[kind] = {k: float(row[k]) for k in ("Calls", "AverageNs", "MinNs", "MaxNs")}
-    lines = ["# Kernel durations: 1B K=8 outer step (24 units x 51,384,320, bf16 replicas)", "",
-             "Command (from the repository root; `<out>` = gpurun_out):", "",
-             "    " + PROFILE_CMDS["trace"], "",
+    lines = [f"# Kernel durations: 1B K=8 {title} (24 units x 51,384,320, bf16 replicas)", "",
+             "Command (from the repository root; `<out>` = the directory the profiler wrote to):", "",
+             "    " + cmds["trace"], "",
              "| kernel | calls | avg us | min us | max us | algorithmic bytes | GB/s at avg |",
              "|---|---|---|---|---|---|---|"]
-    for kind in ("pass1_gram_kernel", "decide_kernel", "pass2_update_kernel"):
+    for kind in kinds:
         st = stats.get(kind)
         if not st:
             continue
@@ -238,19 +261,19 @@ def summarize_profiles(out_dir: str, bench_json: str) -> None:
         lines.append(f"| {kind} | {int(st['Calls'])} | {st['AverageNs'] / 1e3:.1f} | "
                      f"{st['MinNs'] / 1e3:.1f} | {st['MaxNs'] / 1e3:.1f} | {b if b else '-'} | {gbps} |")
     rl = bench.get("roofline") or {}
-    if "pass2_update_kernel" in stats and rl:
+    if dominant in stats and rl:
         ours = rl["avg_launch_ms"] * 1e3
-        prof = stats["pass2_update_kernel"]["AverageNs"] / 1e3
-        lines += ["", f"bench.py's own HIP-event average for pass2_update_kernel (sampled units, same "
-                  f"workload, default run): {ours:.1f} us; rocprofv3: {prof:.1f} us "
-                  f"({100 * (ours - prof) / prof:+.1f}%)."]
-    with open(os.path.join(prof_dir, "c3_kernel_trace_stats.md"), "w") as f:
+        prof = stats[dominant]["AverageNs"] / 1e3
+        lines += ["", f"bench.py's own HIP-event average for {dominant} (sampled units, same "
+                  f"workload, default run{' with --one-pass' if one else ''}): {ours:.1f} us; "
+                  f"rocprofv3: {prof:.1f} us ({100 * (ours - prof) / prof:+.1f}%)."]
+    with open(os.path.join(prof_dir, f"{name}_kernel_trace_stats.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
     # HBM counters, calibrated on the 2 GiB copy probe of the same run
-    def counters(tag):
+    def counters(which):
         per = {}
-        with open(os.path.join(out_dir, f"prof_{tag}", "c3_counter_collection.csv")) as f:
+        with open(os.path.join(out_dir, f"prof_{which}{sfx}", f"{tag}_counter_collection.csv")) as f:
             for row in csv.DictReader(f):
                 kind = _kernel_kind(row["Kernel_Name"])
                 if kind:
@@ -263,18 +286,26 @@ def summarize_profiles(out_dir: str, bench_json: str) -> None:
     copy_write = max(v for (k, g), vals in write.items() if k == "copy_kernel" for v in vals)
     fetch_scale = copy_bytes / (copy_fetch * 1024)
     write_scale = copy_bytes / (copy_write * 1024)
-    out = {"workload": "c3", "kernel_source_sha256_16": kernel_source_hash(),
-           "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4),
-           "commands": [PROFILE_CMDS["fetch"], PROFILE_CMDS["write"]]}
-    lines = ["# HBM traffic counters: 1B K=8 outer step", "",
-             "Commands (from the repository root; `<out>` = gpurun_out):", "",
-             "    " + PROFILE_CMDS["fetch"], "    " + PROFILE_CMDS["write"], "",
+    try:  # keep the other variant's entries when they were taken on this source
+        with open(COUNTERS_FILE) as f:
+            out = json.load(f)
+        if out.get("kernel_source_sha256_16") != kernel_source_hash():
+            out = {}
+    except (OSError, ValueError):
+        out = {}
+    out.update({"workload": "c3", "kernel_source_sha256_16": kernel_source_hash(),
+                f"{variant}_fetch_scale": round(fetch_scale, 4),
+                f"{variant}_write_scale": round(write_scale, 4),
+                f"{variant}_commands": [cmds["fetch"], cmds["write"]]})
+    lines = [f"# HBM traffic counters: 1B K=8 {title}", "",
+             "Commands (from the repository root; `<out>` = the directory the profiler wrote to):", "",
+             "    " + cmds["fetch"], "    " + cmds["write"], "",
              f"Calibration on the plain 2 GiB copy kernel in the same runs: FETCH_SIZE reads "
              f"{copy_fetch:.0f} KiB and WRITE_SIZE {copy_write:.0f} KiB for 2,097,152 KiB moved each "
              f"way, so FETCH_SIZE is scaled by {fetch_scale:.4f} and WRITE_SIZE by {write_scale:.4f}.", "",
              "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled bytes/launch | "
              "algorithmic bytes | ratio |", "|---|---|---|---|---|---|---|"]
-    for kind in ("pass1_gram_kernel", "decide_kernel", "pass2_update_kernel"):
+    for kind in kinds:
         fv = [v for (k, g), vals in fetch.items() if k == kind for v in vals]
         wv = [v for (k, g), vals in write.items() if k == kind for v in vals]
         if not fv or not wv:
@@ -285,19 +316,18 @@ def summarize_profiles(out_dir: str, bench_json: str) -> None:
         ratio = f"{traffic / b:.4f}" if b else "-"
         lines.append(f"| {kind} | {len(fv)} | {f_kib:.1f} | {w_kib:.1f} | {traffic:.4e} | "
                      f"{b if b else '-'} | {ratio} |")
-        short = kind.split("_")[0]
+        short = SHORT[kind]
         out[f"{short}_bytes_per_launch"] = round(traffic)
         out[f"{short}_fetch_kib"] = round(f_kib, 1)
         out[f"{short}_write_kib"] = round(w_kib, 1)
-        if kind in algo_rw:
-            out[f"{short}_algorithmic_bytes"] = algo[kind]
-    with open(os.path.join(prof_dir, "c3_hbm_counters.md"), "w") as f:
+        if b:
+            out[f"{short}_algorithmic_bytes"] = b
+    with open(os.path.join(prof_dir, f"{name}_hbm_counters.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     with open(COUNTERS_FILE, "w") as f:
         json.dump(out, f, indent=1)
         f.write("\n")
     print(json.dumps(out))
-
 
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[1])
@@ -309,6 +339,9 @@ def main(argv=None) -> int:
     ap.add_argument("--per-unit", action="store_true",
                     help="one edit_outer_step_layer call per unit instead of edit_outer_step_round")
     ap.add_argument("--units", type=int, default=0, help="use only the first N units (0 = all)")
+    ap.add_argument("--one-pass", action="store_true",
+                    help="the DiLoCo outer step (no penalty components) as one fused pass "
+                         "(flag EDIT_ONE_PASS)")
     ap.add_argument("--shards", type=int, default=1,
                     help="split every unit into S shards that share one decision through "
                          "edit_outer_gram_layer / edit_outer_apply_layer (the module-norm path)")
@@ -322,11 +355,13 @@ def main(argv=None) -> int:
                     help="skip the untimed cache settle between input generation and the step")
     ap.add_argument("--summarize-profiles", nargs=2, metavar=("OUT_DIR", "BENCH_JSON"),
                     help="write profiles/ summaries from rocprofv3 CSVs under OUT_DIR (no GPU)")
+    ap.add_argument("--profile-variant", default="two-pass", choices=("two-pass", "one-pass"),
+                    help="which step --summarize-profiles reads (default: the two-pass step)")
     ap.add_argument("--summarize-trace", nargs=2, metavar=("OUT_DIR", "WORKLOAD"),
                     help="write a per-unit-size kernel table from a rocprofv3 kernel trace (no GPU)")
     args = ap.parse_args(argv)
     if args.summarize_profiles:
-        summarize_profiles(*args.summarize_profiles)
+        summarize_profiles(*args.summarize_profiles, variant=args.profile_variant)
         return 0
     if args.summarize_trace:
         print(summarize_trace_by_grid(*args.summarize_trace))
@@ -341,7 +376,7 @@ def main(argv=None) -> int:
     import numpy as np
     import torch
 
-    from paper_2412_07210_amd import EditOuter, OuterConfig, outer, synth
+    from paper_2412_07210_amd import ONE_PASS, EditOuter, OuterConfig, outer, synth
 
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}), flush=True)
@@ -358,6 +393,11 @@ def main(argv=None) -> int:
     if S > 1 and (args.per_unit or args.streams > 1):
         print(json.dumps({"error": "--shards runs its own issue order; drop --per-unit/--streams"}))
         return 2
+    if S > 1 and args.one_pass:
+        print(json.dumps({"error": "the one-pass step has no Gram to share between shards"}))
+        return 2
+    if args.one_pass:
+        hyper["flags"] = ONE_PASS
 
     def shard_cuts(n):
         # contiguous shards whose starts are multiples of 8 elements (16-byte aligned views)
@@ -448,11 +488,11 @@ def main(argv=None) -> int:
         for u, (th, b, reps) in enumerate(units):
             st = lib.state_get(u * S)  # every shard of a module holds the same decision
             active = int(np.count_nonzero(st.weight > 0)) if st.clip_coef > 0 else 0
-            b1, b2 = unit_bytes(th.numel(), K, R, active, st.rolled_back)
+            b1, b2 = unit_bytes(th.numel(), K, R, active, st.rolled_back, args.one_pass)
             p1_bytes += b1
             p2_bytes += b2
             step_bytes += b1 + b2
-            nominal_bytes += th.numel() * (3 * K * R + 20)
+            nominal_bytes += th.numel() * ((2 * K * R + 16) if args.one_pass else (3 * K * R + 20))
             masked_total += int(st.anomalous.sum())
             rollbacks += int(st.rolled_back)
             if events and u % args.profile_every == 0:
@@ -499,6 +539,8 @@ def main(argv=None) -> int:
                             "edit_outer_step_layer per unit" if args.per_unit else
                             "edit_outer_step_round" if args.streams <= 1 else "edit_outer_step_layer, streams"),
             "shards_per_unit": S,
+            "penalty": "none: DiLoCo outer step in one pass (EDIT_ONE_PASS)" if args.one_pass else
+                       "anomaly elimination + weighted averaging + clip (Sec. 3.2)",
             "cache_settle_before_step": not args.no_settle,
             "parallelism": "single GPU, K replicas reduced in HBM",
         },
@@ -512,12 +554,29 @@ def main(argv=None) -> int:
         "rollbacks_total": rollbacks,
         "wall_s": round(wall, 1),
     }
-    if events and p2_ms:
+    if events and args.one_pass and p1_ms:
+        per_launch = p1_sample_bytes / len(p1_ms)
+        avg_ms = sum(p1_ms) / len(p1_ms)
+        achieved = per_launch / (avg_ms * 1e-3) / 1e9
+        result["roofline"] = {
+            "kernel": "fused_mean_kernel (one pass: mean + Nesterov + write-back + norms)",
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4),
+            "traffic": measured_traffic("fused"),
+            "bytes_per_launch": int(per_launch),
+            "avg_launch_ms": round(avg_ms, 5),
+            "sampled_launches": len(p1_ms),
+        }
+        result["kernels_ms_avg"] = {"fused_mean": round(avg_ms, 5)}
+    elif events and p2_ms:
         # average over the sampled launches (units 0, k, 2k, ... of every timed step)
         per_launch = p2_sample_bytes / len(p2_ms)
         avg_ms = sum(p2_ms) / len(p2_ms)
         achieved = per_launch / (avg_ms * 1e-3) / 1e9
-        traffic = measured_traffic(per_launch)
+        traffic = measured_traffic("pass2")
         result["roofline"] = {
             "kernel": "pass2_update_kernel (fused average + clip + Nesterov + write-back)",
             "bound": "hbm",
@@ -543,7 +602,7 @@ def main(argv=None) -> int:
     del units
     torch.cuda.empty_cache()
     if samples:
-        result["cpu_baseline"] = cpu_baseline(samples, wl, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(samples, wl, args.cpu_seconds, args.one_pass)
     print(json.dumps(result), flush=True)
     return 0
 
