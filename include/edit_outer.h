@@ -143,6 +143,28 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
                                     float *const *theta, float *const *momentum,
                                     void *const *replicas, void *stream);
 
+/* One outer round, as edit_outer_step_round, with theta_t and the outer
+ * momentum b kept in HOST memory: the memory-saving placement of the outer
+ * optimizer state that the paper describes (Sec. 3.2), so that the device
+ * holds only the K replicas plus a staging ring of three units' theta and b
+ * (allocated on the first call and kept until edit_outer_destroy).  Per unit,
+ * on two library-owned copy streams: theta and b are copied in while the
+ * previous unit computes, the step runs on `stream` from the staging slot,
+ * and theta' and b' are copied back while the next unit computes.  The
+ * kernels are those of the resident step, so results are the same bit for
+ * bit.  The host link bounds it: 8 bytes per element each way.
+ *   theta_host    [count] host pointers to [n] fp32 theta_t -> theta_{t+1}
+ *   momentum_host [count] host pointers to [n] fp32 b -> b'
+ *                 both must be page-locked (hipHostMalloc), else EDIT_EINVAL
+ *   replicas      [count * K] device pointers, as in edit_outer_step_round
+ * Everything is enqueued behind `stream`'s earlier work, and `stream` waits
+ * for the last copy back: after synchronising `stream` the host arrays hold
+ * theta_{t+1} and b'.  The caller must not touch them before that.  Rounds on
+ * one handle must be issued from one stream. */
+edit_status_t edit_outer_step_round_host(edit_outer_t h, int32_t count, const int32_t *layers,
+                                         float *const *theta_host, float *const *momentum_host,
+                                         void *const *replicas, void *stream);
+
 /* A module whose parameters are sharded over several devices (the model-shard
  * group of Sec. 3.1) still takes its penalty on norms of the WHOLE module
  * (Sec. 3.2): each shard contributes partial sums, which the shards add up

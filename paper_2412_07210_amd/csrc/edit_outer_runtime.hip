@@ -47,6 +47,27 @@ struct Unit {
 
 }  // namespace
 
+namespace {
+
+// Staging of theta and momentum for rounds whose master copies live in host
+// memory: a ring of device slots, one stream per copy direction, and per
+// slot the events that order copy-in -> compute -> copy-out -> reuse.
+constexpr int kOffloadSlots = 3;
+
+struct Offload {
+  int64_t cap = 0;           // elements per slot (theta and b each)
+  float* buf = nullptr;      // [kOffloadSlots][2][cap] fp32
+  hipStream_t h2d = nullptr, d2h = nullptr;
+  hipEvent_t in_done[kOffloadSlots] = {};
+  hipEvent_t comp_done[kOffloadSlots] = {};
+  hipEvent_t out_done[kOffloadSlots] = {};
+  hipEvent_t start = nullptr;  // the caller's stream at the start of a round
+  bool used[kOffloadSlots] = {};
+  bool ready = false;
+};
+
+}  // namespace
+
 struct edit_outer {
   edit_outer_config_t cfg{};
   std::vector<int64_t> numel;
@@ -57,6 +78,7 @@ struct edit_outer {
   char* arena = nullptr;   // one device allocation for every unit's scratch
   FinishEntry* finish_table = nullptr;  // one-pass mode: [L] entries, in the arena
   bool one_pass = false;
+  Offload off;
   std::vector<Unit> units;
 };
 
@@ -77,7 +99,24 @@ edit_status_t check_device(const edit_outer* h) {
   return EDIT_OK;
 }
 
+void destroy_offload(edit_outer* h) {
+  Offload& o = h->off;
+  if (o.h2d) (void)hipStreamSynchronize(o.h2d);
+  if (o.d2h) (void)hipStreamSynchronize(o.d2h);
+  for (int s = 0; s < kOffloadSlots; ++s) {
+    if (o.in_done[s]) (void)hipEventDestroy(o.in_done[s]);
+    if (o.comp_done[s]) (void)hipEventDestroy(o.comp_done[s]);
+    if (o.out_done[s]) (void)hipEventDestroy(o.out_done[s]);
+  }
+  if (o.start) (void)hipEventDestroy(o.start);
+  if (o.h2d) (void)hipStreamDestroy(o.h2d);
+  if (o.d2h) (void)hipStreamDestroy(o.d2h);
+  if (o.buf) (void)hipFree(o.buf);
+  o = Offload{};
+}
+
 void destroy_units(edit_outer* h) {
+  destroy_offload(h);
   for (Unit& u : h->units) {
     if (u.done) (void)hipEventDestroy(u.done);
     for (hipEvent_t& ev : u.prof)
@@ -509,6 +548,145 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
     EDIT_TRY(q.decide(layers[pending]));
     EDIT_TRY(flush_pass2(pending));
   }
+  return EDIT_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Page-locked host memory (hipHostMalloc, or torch's pin_memory), which the
+// copy engines can read and write asynchronously.
+bool is_pinned_host(const void* p) {
+  hipPointerAttribute_t attr;
+  const hipError_t e = hipPointerGetAttributes(&attr, p);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();  // an unregistered pointer is an answer, not a failure
+    return false;
+  }
+  return attr.type == hipMemoryTypeHost;
+}
+
+edit_status_t offload_setup(edit_outer* h) {
+  Offload& o = h->off;
+  if (o.ready) return EDIT_OK;
+  int64_t cap = 64;
+  for (const Unit& u : h->units) cap = std::max(cap, u.n);
+  cap = ceil_div(cap, 64) * 64;  // each half of a slot stays 256-byte aligned
+  hipError_t e = hipMalloc(reinterpret_cast<void**>(&o.buf),
+                           sizeof(float) * 2 * kOffloadSlots * static_cast<size_t>(cap));
+  if (e != hipSuccess) {
+    o.buf = nullptr;
+    return fail(EDIT_ENOMEM, std::string("hipMalloc of the staging ring: ") + hipGetErrorString(e));
+  }
+  o.cap = cap;
+  if ((e = hipStreamCreateWithFlags(&o.h2d, hipStreamNonBlocking)) != hipSuccess ||
+      (e = hipStreamCreateWithFlags(&o.d2h, hipStreamNonBlocking)) != hipSuccess ||
+      (e = hipEventCreateWithFlags(&o.start, hipEventDisableTiming)) != hipSuccess) {
+    destroy_offload(h);
+    return fail_hip(e, "offload streams");
+  }
+  for (int s = 0; s < kOffloadSlots; ++s)
+    if ((e = hipEventCreateWithFlags(&o.in_done[s], hipEventDisableTiming)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&o.comp_done[s], hipEventDisableTiming)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&o.out_done[s], hipEventDisableTiming)) != hipSuccess) {
+      destroy_offload(h);
+      return fail_hip(e, "offload events");
+    }
+  o.ready = true;
+  return EDIT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+edit_status_t edit_outer_step_round_host(edit_outer_t h, int32_t count, const int32_t* layers,
+                                         float* const* theta_host, float* const* momentum_host,
+                                         void* const* replicas, void* stream) {
+  if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  if (count < 1) return fail(EDIT_EINVAL, "count must be >= 1");
+  if (!layers || !theta_host || !momentum_host || !replicas)
+    return fail(EDIT_EINVAL, "layers, theta_host, momentum_host and replicas must not be NULL");
+  EDIT_TRY(check_device(h));
+  EDIT_TRY(offload_setup(h));
+  Offload& o = h->off;
+  const int K = h->cfg.num_workers;
+  std::vector<char> seen(h->cfg.num_layers, 0);
+  for (int32_t i = 0; i < count; ++i) {
+    const int32_t l = layers[i];
+    // the replicas are checked against a staging slot standing in for theta/b
+    EDIT_TRY(check_step(h, l, o.buf, o.buf + o.cap, replicas + static_cast<size_t>(i) * K));
+    if (seen[l]++) return fail(EDIT_EINVAL, "layer " + std::to_string(l) + " appears twice in a round");
+    const int64_t n = h->units[l].n;
+    if (n == 0) continue;
+    const float* th = theta_host[i];
+    const float* mo = momentum_host[i];
+    if (!th || !mo) return fail(EDIT_EINVAL, "theta_host and momentum_host must not be NULL");
+    if (!is_pinned_host(th) || !is_pinned_host(mo))
+      return fail(EDIT_EINVAL, "theta_host and momentum_host of layer " + std::to_string(l) +
+                                   " must be pinned host memory (hipHostMalloc)");
+    const uintptr_t a = reinterpret_cast<uintptr_t>(th), b = reinterpret_cast<uintptr_t>(mo);
+    if (a < b + 4 * n && b < a + 4 * n)
+      return fail(EDIT_EINVAL, "theta_host and momentum_host overlap");
+  }
+  hipStream_t cs = reinterpret_cast<hipStream_t>(stream);
+  Enqueue q{h, cs, decide_params(h), K, h->cfg.replica_dtype == EDIT_BF16};
+  hipError_t e = hipEventRecord(o.start, cs);
+  if (e == hipSuccess) e = hipStreamWaitEvent(o.h2d, o.start, 0);
+  if (e != hipSuccess) return fail_hip(e, "round start");
+  bool used_now[kOffloadSlots] = {};
+  for (int32_t i = 0; i < count; ++i) {
+    const int32_t l = layers[i];
+    Unit& u = h->units[l];
+    const int s = i % kOffloadSlots;
+    float* dth = o.buf + static_cast<size_t>(s) * 2 * o.cap;
+    float* db = dth + o.cap;
+    void* const* reps = replicas + static_cast<size_t>(i) * K;
+    const size_t bytes = sizeof(float) * static_cast<size_t>(u.n);
+    // copy in, once the slot's previous unit has been copied out
+    if (o.used[s] && (e = hipStreamWaitEvent(o.h2d, o.out_done[s], 0)) != hipSuccess)
+      return fail_hip(e, "hipStreamWaitEvent");
+    if (u.n > 0 &&
+        ((e = hipMemcpyAsync(dth, theta_host[i], bytes, hipMemcpyHostToDevice, o.h2d)) != hipSuccess ||
+         (e = hipMemcpyAsync(db, momentum_host[i], bytes, hipMemcpyHostToDevice, o.h2d)) != hipSuccess))
+      return fail_hip(e, "copy to device");
+    if ((e = hipEventRecord(o.in_done[s], o.h2d)) != hipSuccess ||
+        (e = hipStreamWaitEvent(cs, o.in_done[s], 0)) != hipSuccess)
+      return fail_hip(e, "copy-in event");
+    // the step itself, on the caller's stream, from the staging slot
+    EDIT_TRY(q.event(u, l, 0));
+    if (h->one_pass) {
+      EDIT_TRY(q.fused(l, dth, db, reps));
+      EDIT_TRY(q.event(u, l, 1));
+      EDIT_TRY(q.event(u, l, 2));
+      EDIT_TRY(q.records(l, 1));
+    } else {
+      EDIT_TRY(q.pass1(l, dth, reps, nullptr));
+      EDIT_TRY(q.decide(l));
+      EDIT_TRY(q.event(u, l, 1));
+      EDIT_TRY(q.event(u, l, 2));
+      EDIT_TRY(q.pass2(l, dth, db, reps));
+    }
+    EDIT_TRY(q.event(u, l, 3));
+    EDIT_TRY(q.finish(l));
+    // copy out once the step is done
+    if ((e = hipEventRecord(o.comp_done[s], cs)) != hipSuccess ||
+        (e = hipStreamWaitEvent(o.d2h, o.comp_done[s], 0)) != hipSuccess)
+      return fail_hip(e, "compute event");
+    if (u.n > 0 &&
+        ((e = hipMemcpyAsync(theta_host[i], dth, bytes, hipMemcpyDeviceToHost, o.d2h)) != hipSuccess ||
+         (e = hipMemcpyAsync(momentum_host[i], db, bytes, hipMemcpyDeviceToHost, o.d2h)) != hipSuccess))
+      return fail_hip(e, "copy to host");
+    if ((e = hipEventRecord(o.out_done[s], o.d2h)) != hipSuccess) return fail_hip(e, "copy-out event");
+    o.used[s] = true;
+    used_now[s] = true;
+  }
+  // the caller's stream covers the copies back: synchronising it makes the
+  // host arrays current
+  for (int s = 0; s < kOffloadSlots; ++s)
+    if (used_now[s] && (e = hipStreamWaitEvent(cs, o.out_done[s], 0)) != hipSuccess)
+      return fail_hip(e, "round end");
   return EDIT_OK;
 }
 

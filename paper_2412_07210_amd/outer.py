@@ -29,7 +29,7 @@ EDIT_OK, EDIT_EINVAL, EDIT_ENOMEM, EDIT_EHIP, EDIT_ESTATE, EDIT_ENODEV = 0, -1, 
 # Every function the header declares; the CPU tests check the library exports them.
 EXPORTS = (
     "edit_outer_init", "edit_outer_step_layer", "edit_outer_step_round",
-    "edit_outer_gram_layer", "edit_outer_apply_layer",
+    "edit_outer_step_round_host", "edit_outer_gram_layer", "edit_outer_apply_layer",
     "edit_outer_state_get", "edit_outer_state_set",
     "edit_outer_destroy", "edit_outer_strerror", "edit_outer_last_error",
     "edit_outer_set_profiling", "edit_outer_kernel_times", "edit_outer_copy_probe",
@@ -98,6 +98,10 @@ def load_library() -> ctypes.CDLL:
                                           ctypes.POINTER(vp), ctypes.POINTER(vp),
                                           ctypes.POINTER(vp), vp]
     lib.edit_outer_step_round.restype = st
+    lib.edit_outer_step_round_host.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
+                                               ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                               ctypes.POINTER(vp), vp]
+    lib.edit_outer_step_round_host.restype = st
     lib.edit_outer_gram_layer.argtypes = [vp, ctypes.c_int32, vp, ctypes.POINTER(vp), vp, vp]
     lib.edit_outer_gram_layer.restype = st
     lib.edit_outer_apply_layer.argtypes = [vp, ctypes.c_int32, vp, vp, vp, ctypes.POINTER(vp), vp]
@@ -306,11 +310,14 @@ class EditOuter:
                           _stream_handle(stream, self.device)),
                "edit_outer_apply_layer")
 
-    def prepare_round(self, units: Sequence[tuple],
-                      layers: Optional[Sequence[int]] = None) -> "RoundPlan":
+    def prepare_round(self, units: Sequence[tuple], layers: Optional[Sequence[int]] = None,
+                      host: bool = False) -> "RoundPlan":
         """Validate a round's tensors once; RoundPlan.run() then enqueues it
-        with a single edit_outer_step_round call (no per-tensor Python work)."""
-        return RoundPlan(self, units, layers)
+        with a single edit_outer_step_round call (no per-tensor Python work).
+        host=True: theta and momentum of every unit are pinned CPU tensors,
+        stepped through edit_outer_step_round_host; synchronise the stream
+        before reading them."""
+        return RoundPlan(self, units, layers, host)
 
     def step_round(self, units: Sequence[tuple], streams: Optional[List[torch.cuda.Stream]] = None,
                    layers: Optional[Sequence[int]] = None) -> None:
@@ -385,8 +392,9 @@ class RoundPlan:
     must not be reallocated while the plan is used."""
 
     def __init__(self, handle: EditOuter, units: Sequence[tuple],
-                 layers: Optional[Sequence[int]] = None):
+                 layers: Optional[Sequence[int]] = None, host: bool = False):
         layers = list(range(len(units))) if layers is None else list(layers)
+        self._host = host
         if len(layers) != len(units) or not units:
             raise ValueError("need one layer index per unit and at least one unit")
         K = handle.cfg.num_workers
@@ -404,8 +412,17 @@ class RoundPlan:
             n = handle._numel[l]
             if len(reps) != K:
                 raise ValueError(f"expected {K} replicas, got {len(reps)}")
-            handle._check_tensor(t, n, torch.float32, "theta")
-            handle._check_tensor(b, n, torch.float32, "momentum")
+            if host:  # theta and momentum in page-locked host memory
+                for x, what in ((t, "theta"), (b, "momentum")):
+                    if not isinstance(x, torch.Tensor) or x.device.type != "cpu":
+                        raise ValueError(f"{what} must be a CPU tensor for a host round")
+                    if x.dtype != torch.float32 or not x.is_contiguous() or x.numel() != n:
+                        raise ValueError(f"{what} must be contiguous float32 with {n} elements")
+                    if n and not x.is_pinned():
+                        raise ValueError(f"{what} must be pinned (torch.empty(..., pin_memory=True))")
+            else:
+                handle._check_tensor(t, n, torch.float32, "theta")
+                handle._check_tensor(b, n, torch.float32, "momentum")
             for j, r in enumerate(reps):
                 handle._check_tensor(r, n, handle.cfg.torch_dtype, f"replicas[{j}]")
                 self._reps[i * K + j] = r.data_ptr()
@@ -414,14 +431,9 @@ class RoundPlan:
     def run(self, stream: Optional[torch.cuda.Stream] = None) -> None:
         h = self._handle
         s = _stream_handle(stream, h.device)
-        if torch.cuda.current_device() != h.device.index:
-            with torch.cuda.device(h.device):
-                status = h._lib.edit_outer_step_round(h._h, self._count, self._layers, self._theta,
-                                                      self._mom, self._reps, s)
-        else:
-            status = h._lib.edit_outer_step_round(h._h, self._count, self._layers, self._theta,
-                                                  self._mom, self._reps, s)
-        _check(status, "edit_outer_step_round")
+        name = "edit_outer_step_round_host" if self._host else "edit_outer_step_round"
+        fn = getattr(h._lib, name)
+        _check(h._call(fn, self._count, self._layers, self._theta, self._mom, self._reps, s), name)
 
 
 def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream: Optional[torch.cuda.Stream] = None) -> None:

@@ -93,6 +93,7 @@ def test_null_arguments_are_rejected():
     assert lib.edit_outer_init(None, ctypes.byref(h)) == outer.EDIT_EINVAL
     assert lib.edit_outer_step_layer(None, 0, None, None, None, None) == outer.EDIT_EINVAL
     assert lib.edit_outer_step_round(None, 1, None, None, None, None, None) == outer.EDIT_EINVAL
+    assert lib.edit_outer_step_round_host(None, 1, None, None, None, None, None) == outer.EDIT_EINVAL
     assert lib.edit_outer_gram_layer(None, 0, None, None, None, None) == outer.EDIT_EINVAL
     assert lib.edit_outer_apply_layer(None, 0, None, None, None, None, None) == outer.EDIT_EINVAL
     assert lib.edit_outer_state_get(None, 0, None) == outer.EDIT_EINVAL
