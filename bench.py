@@ -28,6 +28,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
+PEAK_HOST_LINK_GBPS = 64.0  # PCIe 5.0 x16 host interface, per direction, published
 METRIC = "outer-sync ms/step and achieved HBM GB/s (% of peak), 1B model K=8"
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2412_07210_amd", "csrc", "edit_outer_kernels.hip")
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_counters.json")
@@ -92,6 +93,32 @@ def copy_probe_gbps(torch, outer, nbytes: int = 2 << 30, reps: int = 5) -> float
     ms = a.elapsed_time(b) / reps
     del src, dst
     return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def host_link_probe_gbps(torch, nbytes: int = 1 << 30, reps: int = 3) -> dict:
+    """Pinned host <-> device copy rates (GB/s) of plain torch copies, one
+    direction at a time and both at once on two streams: the practical
+    ceiling of the host-state round."""
+    h = torch.empty(nbytes // 4, dtype=torch.float32, pin_memory=True)
+    h2 = torch.empty_like(h, pin_memory=True)
+    d = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda")
+    d2 = torch.empty_like(d)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    out = {}
+    for name, both in (("h2d", False), ("d2h", False), ("both_each_way", True)):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            if name == "h2d" or both:
+                with torch.cuda.stream(s1):
+                    d.copy_(h, non_blocking=True)
+            if name == "d2h" or both:
+                with torch.cuda.stream(s2):
+                    h2.copy_(d2, non_blocking=True)
+        torch.cuda.synchronize()
+        out[name] = round(nbytes * reps / (time.perf_counter() - t0) / 1e9, 2)
+    del h, h2, d, d2
+    return out
 
 
 def cpu_baseline(samples, wl, seconds_hint: float, one_pass: bool = False):
@@ -342,6 +369,9 @@ def main(argv=None) -> int:
     ap.add_argument("--one-pass", action="store_true",
                     help="the DiLoCo outer step (no penalty components) as one fused pass "
                          "(flag EDIT_ONE_PASS)")
+    ap.add_argument("--host-state", action="store_true",
+                    help="theta and momentum in pinned host memory, stepped through "
+                         "edit_outer_step_round_host (the outer optimizer state off the GPU)")
     ap.add_argument("--shards", type=int, default=1,
                     help="split every unit into S shards that share one decision through "
                          "edit_outer_gram_layer / edit_outer_apply_layer (the module-norm path)")
@@ -398,6 +428,9 @@ def main(argv=None) -> int:
         return 2
     if args.one_pass:
         hyper["flags"] = ONE_PASS
+    if args.host_state and (S > 1 or args.per_unit or args.streams > 1):
+        print(json.dumps({"error": "--host-state runs whole rounds; drop --shards/--per-unit/--streams"}))
+        return 2
 
     def shard_cuts(n):
         # contiguous shards whose starts are multiples of 8 elements (16-byte aligned views)
@@ -414,10 +447,18 @@ def main(argv=None) -> int:
     for u in range(wl.num_units):
         th = wl.init_theta(u, dev, args.seed)
         reps = [torch.empty(th.numel(), dtype=wl.torch_dtype, device=dev) for _ in range(K)]
-        units.append((th, torch.zeros_like(th), reps))
+        if args.host_state:  # the outer optimizer state lives in pinned host memory
+            th_h = torch.empty(th.numel(), dtype=torch.float32, pin_memory=True)
+            th_h.copy_(th)
+            b_h = torch.zeros(th.numel(), dtype=torch.float32, pin_memory=True)
+            del th
+            units.append((th_h, b_h, reps))
+        else:
+            units.append((th, torch.zeros_like(th), reps))
     torch.cuda.synchronize()
     streams = [torch.cuda.Stream(device=dev) for _ in range(args.streams)] if args.streams > 1 else None
-    plan = lib.prepare_round(units) if S == 1 else None  # validated once; each step is one C call
+    # validated once; each step is one C call
+    plan = lib.prepare_round(units, host=args.host_state) if S == 1 else None
     shard_views = []  # per unit: [(handle layer, theta, momentum, replicas)] and its Gram buffers
     for u, (th, b, reps) in enumerate(units):
         cuts = shard_cuts(th.numel())
@@ -457,7 +498,7 @@ def main(argv=None) -> int:
     for t in range(total_rounds):
         std = wl.worker_std(t, args.seed)
         for u, (th, b, reps) in enumerate(units):
-            wl.fill_replicas(th, reps, u, t, args.seed, std=std)
+            wl.fill_replicas(th.to(dev) if args.host_state else th, reps, u, t, args.seed, std=std)
         timed = t >= args.warmup
         if timed and t == args.warmup and not args.no_cpu_baseline:
             for u in range(min(3, wl.num_units)):
@@ -539,6 +580,7 @@ def main(argv=None) -> int:
                             "edit_outer_step_layer per unit" if args.per_unit else
                             "edit_outer_step_round" if args.streams <= 1 else "edit_outer_step_layer, streams"),
             "shards_per_unit": S,
+            "entry_point_host_state": "edit_outer_step_round_host" if args.host_state else None,
             "penalty": "none: DiLoCo outer step in one pass (EDIT_ONE_PASS)" if args.one_pass else
                        "anomaly elimination + weighted averaging + clip (Sec. 3.2)",
             "cache_settle_before_step": not args.no_settle,
@@ -596,6 +638,23 @@ def main(argv=None) -> int:
         }
     else:
         result["roofline"] = None
+    if args.host_state:
+        # Bound by the host link: theta and b cross it once each way per step.
+        each_way = sum(th.numel() for th, _, _ in units) * 8
+        achieved = each_way / (ms_per_step * 1e-3) / 1e9
+        result["config"]["state_placement"] = "theta, momentum in pinned host memory; replicas in HBM"
+        result["hbm_kernels_roofline"] = result["roofline"]
+        result["roofline"] = {
+            "kernel": "staging copies of theta and b (hipMemcpyAsync on two copy streams)",
+            "bound": "host-link",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_HOST_LINK_GBPS,
+            "unit": "GB/s each way",
+            "frac": round(achieved / PEAK_HOST_LINK_GBPS, 4),
+            "traffic": None,
+            "bytes_per_step_each_way": each_way,
+        }
+        result["host_link_probe_gbps"] = host_link_probe_gbps(torch)
     if not args.no_copy_probe:
         result["copy_probe_gbps"] = round(copy_probe_gbps(torch, outer), 1)
     lib.close()
