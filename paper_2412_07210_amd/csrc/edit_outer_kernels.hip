@@ -166,39 +166,55 @@ __device__ __forceinline__ int pair_index(int K, int j, int k) {  // j <= k
 // ------------------------------------------------------------- decision
 
 constexpr int kDecideThreads = 1024;  // one block; wide so the partial loads overlap
-constexpr int kReduceWaves = 16;      // logical waves of the partial reduction
+constexpr int kReduceLogical = 1024;  // logical threads of the partial reduction
 
 // Reduce the per-block Gram partials [NP][rows] in a fixed order into
-// gram[NP] (shared memory).  Called by every thread of one block of
-// kBlockThreads; the sums (16 logical waves, lane r takes rows r, r+64, ...,
-// then a butterfly) depend on neither the block size nor the unrolling, so a
-// standalone decision kernel and one folded into a pass-1 launch agree bit
-// for bit.
-template <int K, int kBlockThreads, int kUnrollRows>
-__device__ void reduce_partials(const double* partials, int rows, double* gram) {
+// gram[NP] (shared memory).  Logical thread lt takes pair lt / T and rows
+// lt % T, lt % T + T, ... (T phases per pair, at most 64), with 16 loads in
+// flight, and the T phase sums of a pair are then added in phase order.
+// The partials were just written by every XCD's blocks, so the loads come
+// from the Infinity Cache or HBM and the reduction is latency-bound: many
+// independent loads per thread matter more than anything else here.  The
+// order depends on neither the block size nor the unrolling, so a standalone
+// decision kernel, one folded into a pass-1 launch and the Gram export agree
+// bit for bit.  `scratch` holds kReduceLogical doubles of shared memory.
+template <int K, int kBlockThreads>
+__device__ void reduce_partials(const double* partials, int rows, double* gram, double* scratch) {
   constexpr int NP = K * (K + 1) / 2;
-  constexpr int PPW = (NP + kReduceWaves - 1) / kReduceWaves;  // pairs per logical wave
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  for (int vw = wave; vw < kReduceWaves; vw += kBlockThreads / 64) {
-    double s[PPW];
-#pragma unroll
-    for (int q = 0; q < PPW; ++q) s[q] = 0.0;
-#pragma unroll kUnrollRows
-    for (int r = lane; r < rows; r += 64) {
-#pragma unroll
-      for (int q = 0; q < PPW; ++q) {
-        const int p = vw + kReduceWaves * q;
-        if (p < NP) s[q] += __builtin_nontemporal_load(partials + static_cast<int64_t>(p) * rows + r);
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < PPW; ++q) {
-      const int p = vw + kReduceWaves * q;
-      const double t = wave_sum(s[q]);
-      if (lane == 0 && p < NP) gram[p] = t;
-    }
+  constexpr int T = kReduceLogical / NP < 64 ? kReduceLogical / NP : 64;
+  for (int lt = threadIdx.x; lt < NP * T; lt += kBlockThreads) {
+    const int p = lt / T, ph = lt % T;
+    const double* src = partials + static_cast<int64_t>(p) * rows;
+    double acc = 0.0;
+#pragma unroll 16
+    for (int r = ph; r < rows; r += T) acc += __builtin_nontemporal_load(src + r);
+    scratch[lt] = acc;
   }
+  __syncthreads();
+  for (int p = threadIdx.x; p < NP; p += kBlockThreads) {
+    double g = 0.0;
+    for (int ph = 0; ph < T; ++ph) g += scratch[p * T + ph];
+    gram[p] = g;
+  }
+}
+
+// The state a decision starts from: round counter and each worker's EMA
+// pair, loaded by the deciding wave before the partial reduction so that
+// their latency hides behind it.
+struct DecideState {
+  int64_t round;
+  double mu, sigma;  // of the lane's worker (lane < K)
+};
+
+template <int K>
+__device__ __forceinline__ DecideState load_decide_state(const UnitRecord* rec) {
+  const int lane = threadIdx.x & 63;
+  DecideState st{rec->round, 0.0, 0.0};
+  if (lane < K) {
+    st.mu = rec->mu[lane];
+    st.sigma = rec->sigma[lane];
+  }
+  return st;
 }
 
 // The decision of one step from the unit's Gram matrix, taken by one wave:
@@ -206,12 +222,13 @@ __device__ void reduce_partials(const double* partials, int rows, double* gram) 
 // cross-lane steps (min, sums, first contributing worker) are fixed-order
 // butterflies and ballots, so the result is reproducible bit for bit.
 template <int K>
-__device__ void decide(const double* gram, UnitRecord* rec, const DecideParams& prm) {
+__device__ void decide(const double* gram, UnitRecord* rec, const DecideParams& prm,
+                       const DecideState& st) {
   const int lane = threadIdx.x & 63;
   const bool ae = prm.flags & EDIT_AE;
   const bool wa = prm.flags & EDIT_WA;
   const bool gc = prm.flags & EDIT_GC;
-  const int64_t t = rec->round;
+  const int64_t t = st.round;
   const bool z_test = ae && t >= prm.warmup;
   const bool mine = lane < K;
 
@@ -223,8 +240,8 @@ __device__ void decide(const double* gram, UnitRecord* rec, const DecideParams& 
   if (mine) {
     G = sqrt(gram[pair_index(K, lane, lane)]);
     bad = !isfinite(G);
-    const double mu0 = rec->mu[lane];
-    const double sg0 = rec->sigma[lane];
+    const double mu0 = st.mu;
+    const double sg0 = st.sigma;
     if (z_test && !bad) bad = (G - mu0) > prm.delta * sg0;
     rec->norm[lane] = G;
     rec->anomalous[lane] = bad ? 1 : 0;
@@ -301,13 +318,23 @@ struct PrevDecide {
   UnitRecord* rec;
 };
 
+// Threads per block of the Gram pass: every wave a CU holds of it in one
+// block (the VALU version runs 2 waves per SIMD at K = 8, the MFMA version
+// 3), so the block reduction combines them all and the decision kernel
+// reduces one partial row per CU instead of one per 4 waves.
 template <int K>
+constexpr int pass1_threads() {
+  return K <= 8 ? 512 : 768;
+}
+
+template <int K, int kBlockThreads>
 __device__ void run_prev_decide(const PrevDecide& prev, const DecideParams& prm) {
   __shared__ double gram[K * (K + 1) / 2];
-  // not unrolled: this code shares the pass-1 kernel's register budget
-  reduce_partials<K, kThreads, 1>(prev.partials, prev.rows, gram);
+  __shared__ double scratch[kReduceLogical];
+  const DecideState st = load_decide_state<K>(prev.rec);
+  reduce_partials<K, kBlockThreads>(prev.partials, prev.rows, gram, scratch);
   __syncthreads();
-  if (threadIdx.x < 64) decide<K>(gram, prev.rec, prm);
+  if (threadIdx.x < 64) decide<K>(gram, prev.rec, prm, st);
 }
 
 
@@ -345,7 +372,7 @@ __device__ __forceinline__ void load_pass1(const float* theta, const ConstPtrs<K
 }
 
 template <int K, bool BF16, bool NT>
-__global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __restrict__ theta,
+__global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_kernel(const float* __restrict__ theta,
                                                               ConstPtrs<K> reps, int64_t nvec,
                                                               int64_t n,
                                                               double* __restrict__ partials,
@@ -354,7 +381,7 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
   constexpr int VE = Vec<BF16>::VE;
   const int first = prev.partials ? 1 : 0;  // block 0 may take the previous unit's decision
   if (first && blockIdx.x == 0) {
-    run_prev_decide<K>(prev, prm);
+    run_prev_decide<K, pass1_threads<K>()>(prev, prm);
     return;
   }
   const int b = static_cast<int>(blockIdx.x) - first;  // this block's partial row
@@ -367,8 +394,8 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
 #pragma unroll
   for (int p = 0; p < NP; ++p) acc[p] = 0.0;
 
-  const int64_t stride = static_cast<int64_t>(rows) * kThreads;
-  int64_t v = static_cast<int64_t>(b) * kThreads + threadIdx.x;
+  const int64_t stride = static_cast<int64_t>(rows) * pass1_threads<K>();
+  int64_t v = static_cast<int64_t>(b) * pass1_threads<K>() + threadIdx.x;
   // Double-buffered grid-stride loop: buffer A holds trip t, B trip t+1.
   float thA[VE], thB[VE];
   u32x4 rA[K], rB[K];
@@ -398,7 +425,7 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
   }
 
   // Block reduction: wave butterfly, then the four waves in order.
-  __shared__ double red[kThreads / 64][NP];
+  __shared__ double red[pass1_threads<K>() / 64][NP];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
 #pragma unroll
@@ -407,10 +434,10 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_kernel(const float* __res
     if (lane == 0) red[wave][p] = s;
   }
   __syncthreads();
-  for (int p = threadIdx.x; p < NP; p += kThreads) {
+  for (int p = threadIdx.x; p < NP; p += pass1_threads<K>()) {
     double s = red[0][p];
 #pragma unroll
-    for (int w = 1; w < kThreads / 64; ++w) s += red[w][p];
+    for (int w = 1; w < pass1_threads<K>() / 64; ++w) s += red[w][p];
     partials[static_cast<int64_t>(p) * rows + b] = s;
   }
 }
@@ -486,7 +513,7 @@ __device__ __forceinline__ void gram_mfma(f64x4& acc0, f64x4& acc1, const u32x4&
 }
 
 template <int K, bool BF16, bool NT>
-__global__ __launch_bounds__(kThreads) void pass1_gram_mfma_kernel(const float* __restrict__ theta,
+__global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_mfma_kernel(const float* __restrict__ theta,
                                                                    ConstPtrs<K> reps, int64_t nvec,
                                                                    int64_t n,
                                                                    double* __restrict__ partials,
@@ -495,15 +522,23 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_mfma_kernel(const float* 
   static_assert(K > 8 && K <= 16, "MFMA Gram pass covers 8 < K <= 16");
   const int first = prev.partials ? 1 : 0;  // block 0 may take the previous unit's decision
   if (first && blockIdx.x == 0) {
-    run_prev_decide<K>(prev, prm);
+    run_prev_decide<K, pass1_threads<K>()>(prev, prm);
     return;
   }
   const int b = static_cast<int>(blockIdx.x) - first;  // this block's partial row
   const int rows = static_cast<int>(gridDim.x) - first;
   constexpr int NP = K * (K + 1) / 2;
   constexpr int VE = Vec<BF16>::VE;
-  constexpr int kWaves = kThreads / 64;
-  constexpr int V = 2;  // vectors per lane per group: a group is 4*V consecutive vectors
+  constexpr int kWaves = pass1_threads<K>() / 64;
+  // Vectors per lane per group (a group is 4*V consecutive vectors of every
+  // worker).  A wave instruction reads 64 bytes of each of 16 workers, half a
+  // cache line; with cached loads the other half is an L2 hit, where
+  // non-temporal loads fetched it again (measured at K = 16, 51.4M elements:
+  // 380 us for the loads alone cached, 480 us non-temporal).  The kernel as a
+  // whole is bound by the fp64 MFMA rate instead: 256 products per element
+  // (the symmetric half is computed too) at the ~48 TFLOP/s this instruction
+  // sustains here, about 550 us for that unit.
+  constexpr int V = 4;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int w = lane & 15;
@@ -552,7 +587,7 @@ __global__ __launch_bounds__(kThreads) void pass1_gram_mfma_kernel(const float* 
 #pragma unroll
   for (int r = 0; r < 4; ++r) gsh[wave][slot + 4 * r][w] = acc[r];
   __syncthreads();
-  for (int p = threadIdx.x; p < NP; p += kThreads) {
+  for (int p = threadIdx.x; p < NP; p += pass1_threads<K>()) {
     int j = 0, left = p;
     while (left >= K - j) {
       left -= K - j;
@@ -573,9 +608,11 @@ __global__ __launch_bounds__(kDecideThreads) void decide_kernel(const double* __
                                                                 int rows, UnitRecord* __restrict__ rec,
                                                                 DecideParams prm) {
   __shared__ double gram[K * (K + 1) / 2];
-  reduce_partials<K, kDecideThreads, 4>(partials, rows, gram);
+  __shared__ double scratch[kReduceLogical];
+  const DecideState st = load_decide_state<K>(rec);
+  reduce_partials<K, kDecideThreads>(partials, rows, gram, scratch);
   __syncthreads();
-  if (threadIdx.x < 64) decide<K>(gram, rec, prm);
+  if (threadIdx.x < 64) decide<K>(gram, rec, prm, st);
 }
 
 // The Gram of one unit as a plain vector (upper triangle, row by row): the
@@ -587,7 +624,8 @@ __global__ __launch_bounds__(kDecideThreads) void gram_reduce_kernel(const doubl
                                                                      int rows,
                                                                      double* __restrict__ gram_out) {
   __shared__ double gram[K * (K + 1) / 2];
-  reduce_partials<K, kDecideThreads, 4>(partials, rows, gram);
+  __shared__ double scratch[kReduceLogical];
+  reduce_partials<K, kDecideThreads>(partials, rows, gram, scratch);
   __syncthreads();
   for (int p = threadIdx.x; p < K * (K + 1) / 2; p += kDecideThreads) gram_out[p] = gram[p];
 }
@@ -598,9 +636,10 @@ __global__ __launch_bounds__(64) void decide_gram_kernel(const double* __restric
                                                          UnitRecord* __restrict__ rec,
                                                          DecideParams prm) {
   __shared__ double gram[K * (K + 1) / 2];
+  const DecideState st = load_decide_state<K>(rec);
   for (int p = threadIdx.x; p < K * (K + 1) / 2; p += 64) gram[p] = gram_in[p];
   __syncthreads();
-  decide<K>(gram, rec, prm);
+  decide<K>(gram, rec, prm, st);
 }
 
 // ---------------------------------------------------------------- pass 2
@@ -923,6 +962,7 @@ __global__ __launch_bounds__(kThreads) void copy_kernel(u32x4* __restrict__ dst,
 // Cache policy of the streaming kernels: both passes touch every byte once;
 // non-temporal accesses measured ~15% faster for pass 1 and ~5% for pass 2.
 constexpr bool kNT1 = true;
+constexpr bool kNTMfma = false;  // see pass1_gram_mfma_kernel
 constexpr bool kNT2 = true;
 constexpr int kUnrollCopy = 1;
 constexpr bool kNTCopy = false;
@@ -935,7 +975,7 @@ constexpr auto pass1_kernel() {
   if constexpr (K <= 8)
     return pass1_gram_kernel<K, BF16, kNT1>;
   else
-    return pass1_gram_mfma_kernel<K, BF16, kNT1>;
+    return pass1_gram_mfma_kernel<K, BF16, kNTMfma>;
 }
 
 template <int K, bool BF16>
@@ -947,7 +987,7 @@ hipError_t pass1_launch(int rows, const float* theta, const void* const* reps, i
   const int64_t nvec = n / Vec<BF16>::VE;
   const PrevDecide prev{prev_partials, prev_rows, prev_rec};
   const int blocks = rows + (prev_partials ? 1 : 0);
-  hipLaunchKernelGGL((pass1_kernel<K, BF16>()), dim3(blocks), dim3(kThreads), 0, stream, theta, rp,
+  hipLaunchKernelGGL((pass1_kernel<K, BF16>()), dim3(blocks), dim3(pass1_threads<K>()), 0, stream, theta, rp,
                      nvec, n, partials, prev, prm);
   return hipGetLastError();
 }
@@ -1010,9 +1050,9 @@ hipError_t fused_finish_launch(const FinishEntry* table, int units, hipStream_t 
 }
 
 template <typename Kern>
-int occupancy(Kern kernel) {
+int occupancy(Kern kernel, int threads) {
   int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, kThreads, 0) != hipSuccess ||
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, threads, 0) != hipSuccess ||
       blocks < 1)
     blocks = 1;
   return blocks;
@@ -1134,7 +1174,8 @@ int pass1_blocks_per_cu(int K, bool bf16) {
   switch (K) {
 #define EDIT_CASE(KK)                                                          \
   case KK:                                                                     \
-    return bf16 ? occupancy(pass1_kernel<KK, true>()) : occupancy(pass1_kernel<KK, false>());
+    return bf16 ? occupancy(pass1_kernel<KK, true>(), pass1_threads<KK>())       \
+                : occupancy(pass1_kernel<KK, false>(), pass1_threads<KK>());
     EDIT_FOR_EACH_K(EDIT_CASE)
 #undef EDIT_CASE
     default:
