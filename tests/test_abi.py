@@ -106,3 +106,43 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(outer, "LIBRARY", str(tmp_path / "missing.so"))
     with pytest.raises(outer.EditOuterError):
         outer.load_library()
+
+
+def test_header_layout_matches_binding(tmp_path):
+    """Compile a C program against include/edit_outer.h and compare every
+    struct size, field offset and constant with the ctypes mirrors."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    cfg_fields = [f for f, _ in outer._Config._fields_]
+    st_fields = [f for f, _ in outer._LayerState._fields_]
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "edit_outer.h"', 'int main(void) {',
+             '  printf("cfg_size %zu\\n", sizeof(edit_outer_config_t));',
+             '  printf("state_size %zu\\n", sizeof(edit_layer_state_t));']
+    lines += [f'  printf("cfg.{f} %zu\\n", offsetof(edit_outer_config_t, {f}));' for f in cfg_fields]
+    lines += [f'  printf("state.{f} %zu\\n", offsetof(edit_layer_state_t, {f}));' for f in st_fields]
+    consts = ["EDIT_MAX_K", "EDIT_AE", "EDIT_WA", "EDIT_GC", "EDIT_ONE_PASS", "EDIT_OK", "EDIT_EINVAL",
+              "EDIT_ENOMEM", "EDIT_EHIP", "EDIT_ESTATE", "EDIT_ENODEV", "EDIT_F32", "EDIT_BF16"]
+    lines += [f'  printf("{c} %ld\\n", (long)({c}));' for c in consts]
+    lines += ['  return 0;', '}']
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    got = dict(line.split() for line in subprocess.run([str(exe)], check=True, capture_output=True,
+                                                       text=True).stdout.splitlines())
+    assert int(got["cfg_size"]) == ctypes.sizeof(outer._Config)
+    assert int(got["state_size"]) == ctypes.sizeof(outer._LayerState)
+    for f in cfg_fields:
+        assert int(got[f"cfg.{f}"]) == getattr(outer._Config, f).offset, f
+    for f in st_fields:
+        assert int(got[f"state.{f}"]) == getattr(outer._LayerState, f).offset, f
+    py = {"EDIT_MAX_K": outer.MAX_K, "EDIT_AE": outer.AE, "EDIT_WA": outer.WA, "EDIT_GC": outer.GC,
+          "EDIT_ONE_PASS": outer.ONE_PASS, "EDIT_OK": outer.EDIT_OK, "EDIT_EINVAL": outer.EDIT_EINVAL,
+          "EDIT_ENOMEM": outer.EDIT_ENOMEM, "EDIT_EHIP": outer.EDIT_EHIP, "EDIT_ESTATE": outer.EDIT_ESTATE,
+          "EDIT_ENODEV": outer.EDIT_ENODEV, "EDIT_F32": outer.F32, "EDIT_BF16": outer.BF16}
+    for c, v in py.items():
+        assert int(got[c]) == v, c
