@@ -205,9 +205,11 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
             regs[kind] = (row.get("VGPR_Count", "?"), row.get("Accum_VGPR_Count", "?"),
                           row.get("LDS_Block_Size", "?"))
 
+    ve = 8 if wl.replica_dtype == "bf16" else 4  # elements per 16-byte replica vector
+
     def unit_of(kind, grid):
         for n in sizes:
-            nvec = -(-n // 8)
+            nvec = -(-n // ve)
             if kind == "pass2_update_kernel" and -(-nvec // 128) * 128 == grid:
                 return n
             if kind.startswith("pass1_gram") and -(-nvec // 256) >= grid // 256 - 1:
@@ -376,7 +378,7 @@ def main(argv=None) -> int:
                     help="split every unit into S shards that share one decision through "
                          "edit_outer_gram_layer / edit_outer_apply_layer (the module-norm path)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--profile-every", type=int, default=6,
+    ap.add_argument("--profile-every", type=int, default=12,
                     help="record per-kernel HIP events on every k-th unit (0: none, roofline then null)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU-baseline time budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
