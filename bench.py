@@ -212,7 +212,8 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
             nvec = -(-n // ve)
             if kind == "pass2_update_kernel" and -(-nvec // 128) * 128 == grid:
                 return n
-            if kind.startswith("pass1_gram") and -(-nvec // 256) >= grid // 256 - 1:
+            tpb = 768 if kind == "pass1_gram_mfma_kernel" else 512  # threads per Gram-pass block
+            if kind.startswith("pass1_gram") and -(-nvec // 256) >= grid // tpb - 1:
                 return n
         return None
 
