@@ -38,9 +38,19 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def kernel_code_hash(text: str) -> str:
+    """Hash of kernel source with comments and whitespace removed: the identity
+    of the code the HBM counters were taken on (a comment edit keeps it)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    text = " ".join(text.split())
+    return hashlib.sha256(text.encode()).hexdigest()[:16]
+
+
 def kernel_source_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    with open(KERNEL_SOURCE) as f:
+        return kernel_code_hash(f.read())
 
 
 def unit_bytes(n: int, K: int, R: int, active: int, rolled_back: bool, one_pass: bool = False) -> tuple:

@@ -26,7 +26,9 @@
  * clip factor and the elementwise update), rounded once when stored.
  *
  * All pointers to tensor data are DEVICE pointers on the device that was
- * current when the handle was created; the caller owns them.  The library
+ * current when the handle was created (except theta and momentum of
+ * edit_outer_step_round_host, which are pinned HOST memory); the caller owns
+ * them.  The library
  * owns the handle, the EMA state, its scratch memory and its events.
  * Every function returns an edit_status_t; nothing is thrown across the ABI.
  * On failure, edit_outer_last_error() returns a message for the calling

@@ -20,15 +20,22 @@
 // Storage is fp32 (theta, b) and fp32/bf16 (replicas); arithmetic is fp64
 // from the exact pseudo gradients on, rounded once when stored.
 //
-// The passes are HBM-bound (2-3 flop per byte at K = 8), so there is no
-// MFMA.  Lanes move 16-byte vectors (global_load_dwordx4).  Pass 1 runs a
-// persistent grid (resident blocks only, grid-stride), so the chip streams
-// one contiguous window of every buffer at a time; each lane double-buffers its
+// The passes are HBM-bound (2-4 flop per byte at K = 8).  Lanes move 16-byte
+// vectors (global_load_dwordx4).  Pass 1 runs a persistent grid of one block
+// per CU holding all the waves the CU runs of it (grid-stride), so the chip
+// streams one contiguous window of every buffer at a time and the decision
+// reduces one partial row per CU; up to K = 8 each lane double-buffers its
 // vectors (the loads of trip t+1 are in flight while trip t is computed), so
 // the fp64 work hides under the memory latency even at 2 waves per SIMD.
+// Above K = 8 the Gram is a rank-n update on the fp64 matrix cores
+// (v_mfma_f64_16x16x4f64), which the VALU could not hold in registers.
 // Pass 2, which writes as much as it reads, instead gives each thread one
 // vector and lets the block dispatcher order the traffic (see there).
-// Reductions go
+//
+// Also here: the Gram export/import of a sharded module (gram_reduce_kernel,
+// decide_gram_kernel), the one-pass mean step used when no penalty component
+// is on (fused_mean_kernel, fused_finish_kernel), and a plain copy kernel for
+// bandwidth and counter calibration.  Reductions go
 // wave shuffle -> LDS -> per-block partial -> one block in a fixed order, so
 // results are bitwise reproducible.
 #include "edit_outer_internal.h"

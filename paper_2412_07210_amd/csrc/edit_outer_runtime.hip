@@ -3,10 +3,12 @@
 // A handle owns, per sync unit: the device record (EMA state + decision),
 // the per-block Gram partials of pass 1, a completion event and (when
 // profiling) four timing events.  A step validates its arguments, enqueues
-// pass1 -> decide -> pass2 on the caller's stream and returns; a round
-// enqueues many units with each unit's decision folded into the next unit's
-// pass-1 launch.  There is no host synchronisation on the step path and no
-// device-to-host traffic.
+// pass1 -> decide -> pass2 on the caller's stream and returns.  A round
+// enqueues many units, small units' decisions folded into the next unit's
+// pass-1 launch; with EDIT_ONE_PASS it enqueues one fused pass per unit and
+// one record launch at the end.  The host-state round adds a staging ring
+// and two copy streams.  There is no host synchronisation on the step path
+// and, apart from the host-state round's copies, no host-device traffic.
 #include <climits>
 #include <cmath>
 #include <cstdio>
