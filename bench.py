@@ -30,6 +30,9 @@ if ROOT not in sys.path:
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
 PEAK_HOST_LINK_GBPS = 64.0  # PCIe 5.0 x16 host interface, per direction, published
 METRIC = "outer-sync ms/step and achieved HBM GB/s (% of peak), 1B model K=8"
+DEFAULT_WORKLOAD = "llama1b-k8-bf16"  # 24 units x 51,384,320 elements, K = 8, bf16 replicas
+WORKLOAD_NAMES = ("linear1m-k4", "llama350m-k8-f32", "llama1b-k8-bf16", "llama7b-half-k8-bf16",
+                  "aedit1b-k16-bf16")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2412_07210_amd", "csrc", "edit_outer_kernels.hip")
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_counters.json")
 
@@ -72,15 +75,16 @@ def unit_bytes(n: int, K: int, R: int, active: int, rolled_back: bool, one_pass:
     return p1, p2
 
 
-def measured_traffic(kernel: str = "pass2"):
+def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch of `kernel` (pass2, fused) from committed rocprofv3
-    counters, if they were taken on the current kernel source; else None."""
+    counters, if they were taken on this workload and on the current kernel
+    code; else None."""
     try:
         with open(COUNTERS_FILE) as f:
             data = json.load(f)
     except (OSError, ValueError):
         return None
-    if data.get("kernel_source_sha256_16") != kernel_source_hash():
+    if data.get("kernel_source_sha256_16") != kernel_source_hash() or data.get("workload") != workload:
         return None
     try:
         return float(data[f"{kernel}_bytes_per_launch"])
@@ -168,7 +172,7 @@ def cpu_baseline(samples, wl, seconds_hint: float, one_pass: bool = False):
 
 def _profile_cmds(variant: str) -> dict:
     """The rocprofv3 commands whose output summarize_profiles reads."""
-    tag, flag = ("c3op", " --one-pass") if variant == "one-pass" else ("c3", "")
+    tag, flag = ("llama1b_onepass", " --one-pass") if variant == "one-pass" else ("llama1b", "")
     sfx = "_op" if variant == "one-pass" else ""
     return {
         "tag": tag, "suffix": sfx,
@@ -201,10 +205,11 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
     from paper_2412_07210_amd import synth
 
     wl = synth.get(name)
+    tag = name.replace("-", "_")  # file-name form of the workload name
     K, R = wl.num_workers, wl.replica_bytes
     sizes = sorted(set(wl.layer_numel))
     groups, regs = {}, {}
-    with open(os.path.join(out_dir, f"prof_trace_{name}", f"{name}_kernel_trace.csv")) as f:
+    with open(os.path.join(out_dir, f"prof_trace_{tag}", f"{tag}_kernel_trace.csv")) as f:
         for row in csv.DictReader(f):
             kind = _kernel_kind(row["Kernel_Name"])
             if not kind or kind == "copy_kernel":
@@ -231,7 +236,7 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
                             "pass2_update_kernel": n * (16 + 2 * K * R)}.get(kind)
     lines = [f"# Kernel durations by unit size: {wl.description}", "",
              "Command (from the repository root; `<out>` = the directory the profiler wrote to):", "",
-             f"    rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace_{name} -o {name} -- "
+             f"    rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace_{tag} -o {tag} -- "
              f"python bench.py --config {name} --steps 10 --warmup 5 --no-cpu-baseline", "",
              f"Summarised with `python bench.py --summarize-trace <out> {name}` (groups the trace's "
              "dispatches by kernel and grid size).", "",
@@ -250,7 +255,7 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
         lines.append(f"- {kind}: {v} VGPR, {a} AGPR, {l} B LDS")
     text = "\n".join(lines) + "\n"
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
-    with open(os.path.join(ROOT, "profiles", f"{name}_kernel_trace_by_unit.md"), "w") as f:
+    with open(os.path.join(ROOT, "profiles", f"{tag}_kernel_trace_by_unit.md"), "w") as f:
         f.write(text)
     return text
 
@@ -268,7 +273,7 @@ def summarize_profiles(out_dir: str, bench_json: str, variant: str = "two-pass")
     kinds = ("fused_mean_kernel", "fused_finish_kernel") if one else \
         ("pass1_gram_kernel", "decide_kernel", "pass2_update_kernel")
     dominant = "fused_mean_kernel" if one else "pass2_update_kernel"
-    wl = synth.get("c3")
+    wl = synth.get(DEFAULT_WORKLOAD)
     n, K, R = wl.layer_numel[0], wl.num_workers, wl.replica_bytes
     algo = {"pass1_gram_kernel": n * (4 + K * R),
             "pass2_update_kernel": n * (8 + K * R + 8 + K * R),
@@ -276,7 +281,7 @@ def summarize_profiles(out_dir: str, bench_json: str, variant: str = "two-pass")
     title = "one-pass mean step (no penalty components)" if one else "outer step"
     prof_dir = os.path.join(ROOT, "profiles")
     os.makedirs(prof_dir, exist_ok=True)
-    name = "c3_one_pass" if one else "c3"
+    name = "llama1b_k8_one_pass" if one else "llama1b_k8"
     with open(bench_json) as f:
         bench = json.load(f)
 
@@ -333,7 +338,7 @@ def summarize_profiles(out_dir: str, bench_json: str, variant: str = "two-pass")
             out = {}
     except (OSError, ValueError):
         out = {}
-    out.update({"workload": "c3", "kernel_source_sha256_16": kernel_source_hash(),
+    out.update({"workload": DEFAULT_WORKLOAD, "kernel_source_sha256_16": kernel_source_hash(),
                 f"{variant}_fetch_scale": round(fetch_scale, 4),
                 f"{variant}_write_scale": round(write_scale, 4),
                 f"{variant}_commands": [cmds["fetch"], cmds["write"]]})
@@ -374,7 +379,8 @@ def main(argv=None) -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=90)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="c3", help="workload: c1..c5")
+    ap.add_argument("--config", default=DEFAULT_WORKLOAD,
+                    help="workload: " + ", ".join(WORKLOAD_NAMES))
     ap.add_argument("--streams", type=int, default=1, help="HIP streams for the unit pipeline")
     ap.add_argument("--per-unit", action="store_true",
                     help="one edit_outer_step_layer call per unit instead of edit_outer_step_round")
@@ -620,7 +626,7 @@ def main(argv=None) -> int:
             "peak": PEAK_HBM_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBPS, 4),
-            "traffic": measured_traffic("fused"),
+            "traffic": measured_traffic("fused", wl.name),
             "bytes_per_launch": int(per_launch),
             "avg_launch_ms": round(avg_ms, 5),
             "sampled_launches": len(p1_ms),
@@ -631,7 +637,7 @@ def main(argv=None) -> int:
         per_launch = p2_sample_bytes / len(p2_ms)
         avg_ms = sum(p2_ms) / len(p2_ms)
         achieved = per_launch / (avg_ms * 1e-3) / 1e9
-        traffic = measured_traffic("pass2")
+        traffic = measured_traffic("pass2", wl.name)
         result["roofline"] = {
             "kernel": "pass2_update_kernel (fused average + clip + Nesterov + write-back)",
             "bound": "hbm",

@@ -65,7 +65,8 @@ class Workload:
     units: Tuple[Tuple[Segment, ...], ...]  # per sync unit, its segments
     delta_std: float                        # base std of a worker's pseudo gradient
     scale_mode: str = "fixed"               # fixed | uniform_0.5_2 | aedit_steps
-    anomaly_mode: str = "none"              # none | c1 | c3 | c5
+    # none | last_x50_from_round_10 | one_x20_every_10_rounds | three_x30_after_warmup
+    anomaly_mode: str = "none"
     rounds: int = 10
     outer_lr: float = 0.8
     momentum: float = 0.85
@@ -114,16 +115,16 @@ class Workload:
     def anomalies(self, round_: int, seed: int = 0) -> Dict[int, float]:
         """Workers whose pseudo gradient is scaled up this round: {worker: factor}."""
         K = self.num_workers
-        if self.anomaly_mode == "c1":
+        if self.anomaly_mode == "last_x50_from_round_10":
             # Ten clean rounds seed the EMA state; then the last worker is x50.
             return {K - 1: 50.0} if round_ >= 10 else {}
-        if self.anomaly_mode == "c3":
+        if self.anomaly_mode == "one_x20_every_10_rounds":
             # One seeded worker x20 in rounds 19, 29, ..., after the warm-up.
             if round_ >= 19 and round_ % 10 == 9:
                 rng = np.random.default_rng(_seed(seed, self.name, round_, "anomaly"))
                 return {int(rng.integers(K)): 20.0}
             return {}
-        if self.anomaly_mode == "c5":
+        if self.anomaly_mode == "three_x30_after_warmup":
             # After the clean warm-up, three seeded workers are x30 every round.
             if round_ >= self.warmup_rounds:
                 rng = np.random.default_rng(_seed(seed, self.name, round_, "anomaly"))
@@ -185,7 +186,7 @@ def _repeat(seg: Sequence[Segment], times: int) -> Tuple[Tuple[Segment, ...], ..
     return tuple(tuple(seg) for _ in range(times))
 
 
-def _c5_units() -> Tuple[Tuple[Segment, ...], ...]:
+def _aedit_units() -> Tuple[Tuple[Segment, ...], ...]:
     layer = llama_layer_segments(2048, 5632)
     units = []
     for _ in range(24):
@@ -198,38 +199,38 @@ def _c5_units() -> Tuple[Tuple[Segment, ...], ...]:
 _HALF_7B = _take_prefix(llama_layer_segments(4096, 11008), 202_383_360 // 2)
 
 WORKLOADS: Dict[str, Workload] = {
-    "c1": Workload(
-        name="c1",
+    "linear1m-k4": Workload(
+        name="linear1m-k4",
         description="linear layer 1024x1024 fp32, K=4, worker 3 x50 after 10 clean rounds",
         num_workers=4, replica_dtype="f32",
         units=((("linear", 1024 * 1024, "matrix"),),),
-        delta_std=1e-3, scale_mode="fixed", anomaly_mode="c1", rounds=11,
+        delta_std=1e-3, scale_mode="fixed", anomaly_mode="last_x50_from_round_10", rounds=11,
         outer_lr=0.7, momentum=0.9, clip_threshold=1.0),
-    "c2": Workload(
-        name="c2",
+    "llama350m-k8-f32": Workload(
+        name="llama350m-k8-f32",
         description="Llama-style 350M: 24 layers, hidden 1024, FFN 2816, fp32 replicas, K=8",
         num_workers=8, replica_dtype="f32",
         units=_repeat(llama_layer_segments(1024, 2816), 24),
         delta_std=1e-3, scale_mode="uniform_0.5_2", rounds=30),
-    "c3": Workload(
-        name="c3",
+    "llama1b-k8-bf16": Workload(
+        name="llama1b-k8-bf16",
         description="Llama-style 1B: 24 layers, hidden 2048, FFN 5632, bf16 replicas, K=8",
         num_workers=8, replica_dtype="bf16",
         units=_repeat(llama_layer_segments(2048, 5632), 24),
-        delta_std=1e-3, scale_mode="uniform_0.5_2", anomaly_mode="c3", rounds=100),
-    "c4": Workload(
-        name="c4",
+        delta_std=1e-3, scale_mode="uniform_0.5_2", anomaly_mode="one_x20_every_10_rounds", rounds=100),
+    "llama7b-half-k8-bf16": Workload(
+        name="llama7b-half-k8-bf16",
         description="Llama-style 7B half shard: 32 layers x 101,191,680, bf16, K=8, clip active",
         num_workers=8, replica_dtype="bf16",
         units=_repeat(_HALF_7B, 32),
         delta_std=5e-4, scale_mode="fixed", rounds=20,
         clip_threshold=0.889),
-    "c5": Workload(
-        name="c5",
+    "aedit1b-k16-bf16": Workload(
+        name="aedit1b-k16-bf16",
         description="A-EDiT round on 1B shapes: 72 units (matrices + two RMSNorm gains per layer), K=16",
         num_workers=16, replica_dtype="bf16",
-        units=_c5_units(),
-        delta_std=1e-3, scale_mode="aedit_steps", anomaly_mode="c5", rounds=20),
+        units=_aedit_units(),
+        delta_std=1e-3, scale_mode="aedit_steps", anomaly_mode="three_x30_after_warmup", rounds=20),
 }
 
 

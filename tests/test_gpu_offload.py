@@ -35,7 +35,7 @@ def test_host_round_matches_resident_round(K, dtype, one_pass):
     non-index order, three rounds: theta, b, replicas and records equal the
     resident round's bit for bit."""
     sizes = [1_000_000, 2048, 7, 3_000_017, 0, 65_536 + 3]
-    wl = synth.small("c3", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=1,
+    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=1,
                      name=f"host{K}{dtype}")
     order = [2, 0, 5, 1, 4, 3]
     flags = {"flags": ONE_PASS} if one_pass else {}
@@ -80,7 +80,7 @@ def test_host_round_matches_oracle():
     from a preset post-warm-up EMA state on both sides, a round in which
     worker 1 is x40 and must be masked.  Each round both sides start from the
     oracle's theta and b (byte-identical inputs)."""
-    wl = synth.small("c3", [300_001, 4099], num_workers=5, replica_dtype="bf16", warmup_rounds=2,
+    wl = synth.small("llama1b-k8-bf16", [300_001, 4099], num_workers=5, replica_dtype="bf16", warmup_rounds=2,
                      clip_threshold=0.2, name="hostpar")
     K = wl.num_workers
     lib = EditOuter(OuterConfig(K, wl.layer_numel, "bf16", ema_warmup_rounds=2,
@@ -125,7 +125,7 @@ def test_host_round_matches_oracle():
 def test_host_round_rejects_pageable_memory():
     """The copies are asynchronous, so theta and b must be page-locked; the
     library checks this itself (here called without the binding's checks)."""
-    wl = synth.small("c3", [4096], num_workers=2, replica_dtype="f32", name="hostbad")
+    wl = synth.small("llama1b-k8-bf16", [4096], num_workers=2, replica_dtype="f32", name="hostbad")
     h = EditOuter(OuterConfig(2, wl.layer_numel, "f32"), DEV)
     try:
         th = np.zeros(4096, np.float32)

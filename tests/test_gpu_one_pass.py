@@ -33,7 +33,7 @@ def _run(run, rounds, **kw):
 def test_one_pass_ragged_sizes(K, dtype):
     """Unit sizes around the 16-byte vector and the block, K = 1..16."""
     sizes = [0, 1, 7, 8, 9, 255, 2049, 100_003, 1_000_005]
-    wl = synth.small("c3", sizes, num_workers=K, replica_dtype=dtype, name=f"onepass{K}{dtype}")
+    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype, name=f"onepass{K}{dtype}")
     recs = _run(ParityRun(wl, range(len(sizes)), DEV, flags=ONE_PASS), range(3))
     for r in recs[-1]:
         assert r["state"].round == 3
@@ -44,13 +44,13 @@ def test_one_pass_ragged_sizes(K, dtype):
 def test_one_pass_full_size_1b_units():
     """Two 51,384,320-element units of the 1B K=8 bf16 workload, in the launch
     configuration of a handle holding all 24 units."""
-    wl = synth.get("c3")
+    wl = synth.get("llama1b-k8-bf16")
     _run(ParityRun(wl, [0, 23], DEV, flags=ONE_PASS), [10, 19])
 
 
 def test_one_pass_full_size_k16():
     """A 51,380,224-element unit and a 2,048-element unit at K = 16."""
-    wl = synth.get("c5")
+    wl = synth.get("aedit1b-k16-bf16")
     _run(ParityRun(wl, [0, 1], DEV, flags=ONE_PASS), [0])
 
 
@@ -66,7 +66,7 @@ def test_one_pass_round_matches_unit_by_unit(K, dtype):
     """A round (fused passes back to back, one batched record launch at the
     end) gives the same bits and records as unit-by-unit calls."""
     sizes = [1_000_000, 2048, 7, 3_000_017, 0, 65_536 + 3]
-    wl = synth.small("c3", sizes, num_workers=K, replica_dtype=dtype, name=f"oproun{K}{dtype}")
+    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype, name=f"oproun{K}{dtype}")
     order = [2, 0, 5, 1, 4, 3]
     results = []
     for mode in ("layer", "round"):
@@ -95,7 +95,7 @@ def test_one_pass_round_matches_unit_by_unit(K, dtype):
 def test_one_pass_nonfinite_is_reported_not_masked():
     """There is no norm before the average in this mode: a NaN in a replica
     reaches theta at that element, and the worker's reported G_j is NaN."""
-    wl = synth.small("c3", [10_000], num_workers=5, name="opnan")
+    wl = synth.small("llama1b-k8-bf16", [10_000], num_workers=5, name="opnan")
     h = EditOuter(OuterConfig(5, wl.layer_numel, "bf16", flags=ONE_PASS), DEV)
     try:
         th, b, reps = _fresh(wl, 0, 0)

@@ -40,12 +40,12 @@ def _expected_ema(wl, u, round_, seed=0):
     return (np.full(K, 1.25 * G), np.full(K, 0.45 * G), round_)
 
 
-# ------------------------------------------------------------------ C1
+# ------------------------------------------- one 1024x1024 linear layer, K = 4
 
 
-def test_c1_linear_layer_all_rounds():
+def test_linear1m_k4_all_rounds():
     """1024x1024 fp32, K = 4: ten clean rounds, then worker 3 x50 is masked."""
-    wl = synth.get("c1")
+    wl = synth.get("linear1m-k4")
     run = ParityRun(wl, [0], DEV)
     recs = _run(run, range(11))
     assert [int(x) for x in recs[10][0]["anomalous"]] == [0, 0, 0, 1]
@@ -61,7 +61,7 @@ def test_c1_linear_layer_all_rounds():
 def test_ragged_sizes(K, dtype):
     """Unit sizes around the 16-byte vector and the 256-thread block, K = 1..16."""
     sizes = [0, 1, 7, 8, 9, 255, 2049, 100_003, 1_000_005]
-    wl = synth.small("c3", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=2,
+    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=2,
                      clip_threshold=0.05, name=f"ragged{K}{dtype}")
     run = ParityRun(wl, range(len(sizes)), DEV)
     std = lambda t: wl.worker_std(t) * (np.where(np.arange(K) == K - 1, 40.0, 1.0) if t == 3 else 1.0)
@@ -78,7 +78,7 @@ def test_ragged_sizes(K, dtype):
 def test_flag_combinations(flags):
     """Every on/off combination of anomaly elimination, weighting and clipping
     (flags = 0 is the DiLoCo outer step)."""
-    wl = synth.small("c3", [300_001, 4096], num_workers=4, warmup_rounds=2, clip_threshold=0.2,
+    wl = synth.small("llama1b-k8-bf16", [300_001, 4096], num_workers=4, warmup_rounds=2, clip_threshold=0.2,
                      name="flags")
     run = ParityRun(wl, [0, 1], DEV, flags=flags)
     K = wl.num_workers
@@ -97,7 +97,7 @@ def test_flag_combinations(flags):
 def test_rollback_when_all_workers_flagged():
     """Every worker x100 after the warm-up: theta and b keep their values,
     all replicas get theta_t back (Sec. 3.2, Algorithm 2)."""
-    wl = synth.small("c3", [65_536 + 3], num_workers=4, warmup_rounds=2, name="rollback")
+    wl = synth.small("llama1b-k8-bf16", [65_536 + 3], num_workers=4, warmup_rounds=2, name="rollback")
     run = ParityRun(wl, [0], DEV)
     try:
         for t in range(2):
@@ -118,7 +118,7 @@ def test_rollback_when_all_workers_flagged():
 def test_nonfinite_worker_is_masked():
     """A NaN in one replica makes its norm non-finite: that worker is masked
     (even during the warm-up) and the others still synchronize."""
-    wl = synth.small("c3", [10_000, 77], num_workers=5, warmup_rounds=5, name="nan")
+    wl = synth.small("llama1b-k8-bf16", [10_000, 77], num_workers=5, warmup_rounds=5, name="nan")
     run = ParityRun(wl, [0, 1], DEV)
     try:
         recs = run.round(0, poison={2: (13, float("nan"))})
@@ -133,18 +133,18 @@ def test_nonfinite_worker_is_masked():
 # ------------------------------------------------------------ full size
 
 
-def test_c2_full_units():
+def test_llama350m_f32_full_units():
     """Llama-350M-shaped units (12,847,104 fp32 elements, K = 8)."""
-    wl = synth.get("c2")
+    wl = synth.get("llama350m-k8-f32")
     units = [0, 23]
     run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 10) for u in units})
     _run(run, [10, 11])
 
 
-def test_c3_full_units_with_anomaly():
+def test_llama1b_bf16_full_units_with_anomaly():
     """Llama-1B-shaped units (51,384,320 elements, bf16 replicas, K = 8),
     rounds 18-19: round 19 has one worker x20, which must be masked."""
-    wl = synth.get("c3")
+    wl = synth.get("llama1b-k8-bf16")
     units = [0, 11]
     run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 18) for u in units})
     recs = _run(run, [18, 19])
@@ -153,18 +153,18 @@ def test_c3_full_units_with_anomaly():
         assert r["anomalous"][bad] == 1
 
 
-def test_c4_full_unit_clip_active():
+def test_llama7b_half_full_unit_clip_active():
     """7B half shard (101,191,680 elements, bf16, K = 8) with phi = 0.889: clipping active."""
-    wl = synth.get("c4")
+    wl = synth.get("llama7b-half-k8-bf16")
     run = ParityRun(wl, [5], DEV, ema_state={5: _expected_ema(wl, 5, 10)})
     recs = _run(run, [10])
     assert recs[0][0]["clip_coef"] < 1.0
 
 
-def test_c5_full_layer_k16():
+def test_aedit1b_k16_full_layer():
     """A-EDiT round on 1B shapes, K = 16: one layer's matrix unit (51,380,224)
     and its two 2,048-element RMSNorm units, three workers x30."""
-    wl = synth.get("c5")
+    wl = synth.get("aedit1b-k16-bf16")
     units = [0, 1, 2]
     run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 10) for u in units})
     recs = _run(run, [10])
@@ -184,7 +184,7 @@ def _fresh_inputs(wl, u, t, dev):
 
 
 def test_bitwise_deterministic():
-    wl = synth.small("c3", [3_000_017], name="det")
+    wl = synth.small("llama1b-k8-bf16", [3_000_017], name="det")
     outs = []
     for _ in range(2):
         h = EditOuter(OuterConfig(wl.num_workers, wl.layer_numel, "bf16"), DEV)
@@ -200,7 +200,7 @@ def test_bitwise_deterministic():
 
 def test_resume_from_saved_state_is_bitwise():
     """20 rounds straight equal 10 rounds, save EMA state, new handle, restore, 10 rounds."""
-    wl = synth.small("c3", [200_003], warmup_rounds=4, name="resume")
+    wl = synth.small("llama1b-k8-bf16", [200_003], warmup_rounds=4, name="resume")
     cfg = OuterConfig(wl.num_workers, wl.layer_numel, "bf16", ema_warmup_rounds=4)
 
     def play(h, th, b, reps, rounds, h_switch=None):
@@ -235,7 +235,7 @@ def test_round_and_streams_match_unit_by_unit(K, dtype):
     several rounds (EMA state carried), units of mixed sizes and a unit order
     that is not the index order."""
     sizes = [1_000_000, 2048, 7, 3_000_017, 0, 65_536 + 3]
-    wl = synth.small("c3", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=1,
+    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=1,
                      name=f"round{K}{dtype}")
     order = [2, 0, 5, 1, 4, 3]
     results = []
@@ -269,7 +269,7 @@ def test_round_and_streams_match_unit_by_unit(K, dtype):
 
 
 def test_round_rejects_repeated_unit():
-    wl = synth.small("c3", [4096, 4096], name="rep")
+    wl = synth.small("llama1b-k8-bf16", [4096, 4096], name="rep")
     h = EditOuter(OuterConfig(wl.num_workers, wl.layer_numel, "bf16"), DEV)
     units = [_fresh_inputs(wl, u, 0, DEV) for u in range(2)]
     with pytest.raises(EditOuterError) as e:
@@ -282,7 +282,7 @@ def test_round_rejects_repeated_unit():
 
 
 def test_step_rejects_bad_arguments():
-    wl = synth.small("c3", [4096, 100], name="api")
+    wl = synth.small("llama1b-k8-bf16", [4096, 100], name="api")
     h = EditOuter(OuterConfig(wl.num_workers, wl.layer_numel, "bf16"), DEV)
     th, b, reps = _fresh_inputs(wl, 0, 0, DEV)
     with pytest.raises(IndexError):

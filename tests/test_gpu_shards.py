@@ -113,7 +113,7 @@ def test_sharded_module_matches_unsplit_oracle(K, dtype, shards):
     """Three-way ragged split, an empty shard, and an 8-element shard.  Two
     warm-up rounds from the zero EMA state, then (from a preset post-warm-up
     state) two rounds in which three workers are x30 and must be masked."""
-    wl = synth.small("c5", [sum(shards)], num_workers=K, replica_dtype=dtype)
+    wl = synth.small("aedit1b-k16-bf16", [sum(shards)], num_workers=K, replica_dtype=dtype)
     rounds = [0, 1, wl.warmup_rounds, wl.warmup_rounds + 1]
     try:
         recs = list(_sharded_rounds(wl, shards, rounds,
@@ -128,7 +128,7 @@ def test_sharded_module_rollback_and_clip():
     """phi small enough to clip; with a one-round warm-up from the zero EMA
     state every worker fails the next z-test, so round 1 rolls back on the
     module norm (and round 2, the state being unchanged, again)."""
-    wl = synth.small("c1", [65536 + 4099], num_workers=4, replica_dtype="bf16",
+    wl = synth.small("linear1m-k4", [65536 + 4099], num_workers=4, replica_dtype="bf16",
                      warmup_rounds=1, clip_threshold=1e-3)
     try:
         recs = list(_sharded_rounds(wl, (65536, 4099), range(3)))
@@ -143,7 +143,7 @@ def test_sharded_module_rollback_and_clip():
 def test_gram_then_apply_is_step_layer_bitwise(K, dtype, n):
     """For an unsplit unit the two-call path is the one-call path, bit for bit:
     a warm-up round, then two rounds with three x30 workers."""
-    wl = synth.small("c5", [n], num_workers=K, replica_dtype=dtype)
+    wl = synth.small("aedit1b-k16-bf16", [n], num_workers=K, replica_dtype=dtype)
     a, b = _lib(wl, [n]), _lib(wl, [n])
     th0 = wl.init_theta(0, DEV)
     tha, thb = th0.clone(), th0.clone()
@@ -180,8 +180,8 @@ def test_full_size_7b_layer_as_two_shards():
     two contiguous halves of 101,191,680 (each the shape of the 7B half-shard
     workload), one round from a preset post-warm-up EMA state: the decision
     covers both halves, and clipping is active."""
-    n_half = synth.get("c4").unit_numel(0)
-    wl = synth.small("c4", [2 * n_half])
+    n_half = synth.get("llama7b-half-k8-bf16").unit_numel(0)
+    wl = synth.small("llama7b-half-k8-bf16", [2 * n_half])
     try:
         recs = list(_sharded_rounds(wl, (n_half, n_half), [wl.warmup_rounds],
                                     ema={wl.warmup_rounds: _preset_ema(wl, 2 * n_half)}))
@@ -191,7 +191,7 @@ def test_full_size_7b_layer_as_two_shards():
 
 
 def test_gram_and_apply_reject_bad_arguments():
-    wl = synth.small("c1", [1024], num_workers=2, replica_dtype="f32")
+    wl = synth.small("linear1m-k4", [1024], num_workers=2, replica_dtype="f32")
     lib = _lib(wl, [1024])
     try:
         th = torch.zeros(1024, device=DEV)
