@@ -325,13 +325,15 @@ struct PrevDecide {
   UnitRecord* rec;
 };
 
-// Threads per block of the Gram pass: every wave a CU holds of it in one
-// block (the VALU version runs 2 waves per SIMD at K = 8, the MFMA version
-// 3), so the block reduction combines them all and the decision kernel
-// reduces one partial row per CU instead of one per 4 waves.
+// Threads per block of the Gram pass.  The MFMA version runs one block per
+// CU holding all its resident waves (3 per SIMD), so the block reduction
+// combines them and the decision reduces one partial row per CU: at K = 16
+// that row count (255 against 767) took the decision from 26 to 12 us.  The
+// VALU version keeps 256-thread blocks: one 512-thread block per CU shortened
+// its decision too, but made the whole 1B step 0.7% slower (same-box A/B).
 template <int K>
 constexpr int pass1_threads() {
-  return K <= 8 ? 512 : 768;
+  return K <= 8 ? 256 : 768;
 }
 
 template <int K, int kBlockThreads>
