@@ -397,6 +397,9 @@ def main(argv=None) -> int:
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--profile-every", type=int, default=12,
                     help="record per-kernel HIP events on every k-th unit (0: none, roofline then null)")
+    ap.add_argument("--records", metavar="PATH",
+                    help="write every unit's decision of every timed round as JSON lines "
+                         "(G, mask, weights, Gbar, beta, EMA state)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU-baseline time budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-probe", action="store_true")
@@ -513,6 +516,7 @@ def main(argv=None) -> int:
     masked_total = rollbacks = 0
     samples = []
     total_rounds = args.warmup + args.steps
+    records = open(args.records, "w") if args.records else None
     t_start = time.time()
     for t in range(total_rounds):
         std = wl.worker_std(t, args.seed)
@@ -555,6 +559,12 @@ def main(argv=None) -> int:
             nominal_bytes += th.numel() * ((2 * K * R + 16) if args.one_pass else (3 * K * R + 20))
             masked_total += int(st.anomalous.sum())
             rollbacks += int(st.rolled_back)
+            if records:
+                records.write(json.dumps({
+                    "round": t, "unit": u, "G": st.norm.tolist(), "mask": st.anomalous.tolist(),
+                    "w": st.weight.tolist(), "gbar": st.synced_norm, "beta": st.clip_coef,
+                    "rolled_back": bool(st.rolled_back), "z_tested": bool(st.z_tested),
+                    "mu": st.ema_mean.tolist(), "sigma": st.ema_std.tolist()}) + "\n")
             if events and u % args.profile_every == 0:
                 k1, k2 = lib.kernel_times(u)
                 p1_ms.append(k1)
@@ -566,6 +576,8 @@ def main(argv=None) -> int:
         if (t - args.warmup) % 10 == 0:
             log(f"round {t}: {step_ms[-1]:.3f} ms")
     wall = time.time() - t_start
+    if records:
+        records.close()
     del settle_src, settle_dst
 
     total_ms = sum(step_ms)

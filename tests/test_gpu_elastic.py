@@ -1,0 +1,61 @@
+"""The worker count changes between rounds (elastic training, Sec. 4.4).
+
+A sync group that loses workers continues with a new handle for the smaller
+K.  The surviving workers keep their EMA statistics: the library's are read
+with edit_outer_state_get and written into the new handle with
+edit_outer_state_set, the oracle's are carried over the same way on the CPU,
+and both sides keep stepping in lock step.  The anomaly test then still
+works on the carried statistics: a worker x50 after the warm-up is masked
+under its new index.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from parity import NearTie, ParityRun
+from paper_2412_07210_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def test_workers_leave_and_the_ema_state_carries_over():
+    # fixed per-worker scale; the last worker is x50 from round 10 (after the
+    # 10-round warm-up)
+    wl8 = synth.small("linear1m-k4", [65_536 + 3, 4099], num_workers=8, name="elastic")
+    run8 = ParityRun(wl8, [0, 1], DEV)
+    try:
+        for t in range(10):
+            run8.round(t, verbose=False)
+    except NearTie as e:
+        run8.close()
+        pytest.skip(str(e))
+    survivors = [0, 1, 3, 5, 6, 7]  # workers 2 and 4 leave; old worker 7 becomes worker 5
+    carried = []
+    for c in run8.cases:
+        st = run8.lib.state_get(run8.index[c.unit])
+        o = c.records[-1]
+        carried.append(dict(gpu=(st.ema_mean[survivors], st.ema_std[survivors], st.round),
+                            oracle=(o["mu"][survivors], o["sigma"][survivors], o["round"]),
+                            theta=c.theta_h.copy(), mom=c.mom_h.copy()))
+        assert st.round == 10
+    run8.close()
+
+    wl6 = dataclasses.replace(wl8, num_workers=len(survivors))
+    run6 = ParityRun(wl6, [0, 1], DEV)
+    try:
+        for c, cs in zip(run6.cases, carried):
+            run6.lib.state_set(run6.index[c.unit], *cs["gpu"])
+            c.oracle.set_state(*cs["oracle"])
+            c.theta_h, c.mom_h = cs["theta"], cs["mom"]
+        recs = [run6.round(t, verbose=False) for t in (10, 11)]
+    except NearTie as e:
+        pytest.skip(str(e))
+    finally:
+        run6.close()
+    for per_round in recs:
+        for r in per_round:
+            assert list(r["anomalous"]) == [0, 0, 0, 0, 0, 1]
+            assert r["state"].round in (11, 12) and r["state"].z_tested
