@@ -63,9 +63,12 @@ def library_path() -> str:
 def _lib():
     global _lib_handle
     if _lib_handle is None:
-        if not os.path.exists(LIBRARY):
+        # EDIT_ORACLE_LIBRARY points the tests at a deliberately broken build
+        # (tests/test_oracle_mutants.py checks that the pins reject it)
+        path = os.environ.get("EDIT_ORACLE_LIBRARY", LIBRARY)
+        if path == LIBRARY and not os.path.exists(LIBRARY):
             build_oracle()
-        lib = ctypes.CDLL(LIBRARY)
+        lib = ctypes.CDLL(path)
         lib.oracle_step.restype = ctypes.c_int
         lib.oracle_step.argtypes = [
             ctypes.POINTER(_Cfg), ctypes.c_int, ctypes.c_int64, ctypes.c_int,
