@@ -32,7 +32,7 @@ PEAK_HOST_LINK_GBPS = 64.0  # PCIe 5.0 x16 host interface, per direction, publis
 METRIC = "outer-sync ms/step and achieved HBM GB/s (% of peak), 1B model K=8"
 DEFAULT_WORKLOAD = "llama1b-k8-bf16"  # 24 units x 51,384,320 elements, K = 8, bf16 replicas
 WORKLOAD_NAMES = ("linear1m-k4", "llama350m-k8-f32", "llama1b-k8-bf16", "llama7b-half-k8-bf16",
-                  "aedit1b-k16-bf16")
+                  "aedit1b-k16-bf16", "paper1b-k8-bf16")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2412_07210_amd", "csrc", "edit_outer_kernels.hip")
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_counters.json")
 

@@ -218,6 +218,14 @@ WORKLOADS: Dict[str, Workload] = {
         num_workers=8, replica_dtype="bf16",
         units=_repeat(llama_layer_segments(2048, 5632), 24),
         delta_std=1e-3, scale_mode="uniform_0.5_2", anomaly_mode="one_x20_every_10_rounds", rounds=100),
+    # The paper's own 1B model (its model-settings table): 32 layers, hidden
+    # 1536, intermediate 4096, i.e. 28,314,624 parameters per layer.
+    "paper1b-k8-bf16": Workload(
+        name="paper1b-k8-bf16",
+        description="the paper's Llama 1B: 32 layers, hidden 1536, FFN 4096, bf16 replicas, K=8",
+        num_workers=8, replica_dtype="bf16",
+        units=_repeat(llama_layer_segments(1536, 4096), 32),
+        delta_std=1e-3, scale_mode="uniform_0.5_2", anomaly_mode="one_x20_every_10_rounds", rounds=100),
     "llama7b-half-k8-bf16": Workload(
         name="llama7b-half-k8-bf16",
         description="Llama-style 7B half shard: 32 layers x 101,191,680, bf16, K=8, clip active",

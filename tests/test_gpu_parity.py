@@ -153,6 +153,19 @@ def test_llama1b_bf16_full_units_with_anomaly():
         assert r["anomalous"][bad] == 1
 
 
+def test_paper1b_full_units_with_anomaly():
+    """The paper's own 1B shape (28,314,624 elements per layer, bf16, K = 8),
+    first and last of its 32 units, round 19 with one worker x20."""
+    wl = synth.get("paper1b-k8-bf16")
+    assert wl.unit_numel(0) == 28_314_624 and wl.num_units == 32
+    units = [0, 31]
+    run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 19) for u in units})
+    recs = _run(run, [19])
+    bad = list(wl.anomalies(19).keys())[0]
+    for r in recs[0]:
+        assert r["anomalous"][bad] == 1 and r["anomalous"].sum() == 1
+
+
 def test_llama7b_half_full_unit_clip_active():
     """7B half shard (101,191,680 elements, bf16, K = 8) with phi = 0.889: clipping active."""
     wl = synth.get("llama7b-half-k8-bf16")
