@@ -1,0 +1,62 @@
+"""Seeded random configurations against the oracle (GPU).
+
+Each case draws K, unit sizes, the replica type, the penalty switches
+(sometimes the one-pass mode), the hyper-parameters (including edge values:
+rho = 0, alpha = 1, delta = 0, phi = 0, a one-round warm-up) and per-round
+worker scales with occasional x30 or x1000 workers, then steps library and
+oracle in lock step for five rounds.  The draws come from a fixed seed, so
+every run checks the same cases.
+"""
+import numpy as np
+import pytest
+
+from parity import NearTie, ParityRun
+from paper_2412_07210_amd import ONE_PASS, synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+CASES = 48
+
+
+def _draw(i):
+    rng = np.random.default_rng(1000 + i)
+    K = int(rng.choice([1, 2, 3, 4, 6, 8, 9, 12, 16]))
+    sizes = [int(x) for x in rng.choice([0, 1, 5, 8, 33, 257, 4099, 65_537, 300_001], size=2)]
+    dtype = str(rng.choice(["f32", "bf16"]))
+    flags = int(rng.integers(0, 10))
+    if flags >= 8:  # one case in five: the one-pass mean step
+        flags = ONE_PASS
+    hyper = dict(
+        outer_lr=float(rng.choice([0.1, 0.8, 1.0, 1.4])),
+        momentum=float(rng.choice([0.0, 0.5, 0.85, 0.99])),
+        clip_threshold=float(rng.choice([0.0, 1e-3, 0.05, 10.0])),
+        clip_eps=float(rng.choice([1e-6, 1e-3])),
+        ema_alpha=float(rng.choice([0.02, 0.3, 1.0])),
+        z_threshold=float(rng.choice([0.0, 1.0, 3.0])),
+        warmup_rounds=int(rng.choice([0, 1, 2, 10])),
+    )
+    return K, sizes, dtype, flags, hyper, rng
+
+
+@pytest.mark.parametrize("i", range(CASES))
+def test_random_configuration(i):
+    K, sizes, dtype, flags, hyper, rng = _draw(i)
+    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype,
+                     name=f"random{i}", **hyper)
+    print(f"case {i}: K={K} sizes={sizes} {dtype} flags={flags} {hyper}", flush=True)
+    run = ParityRun(wl, range(len(sizes)), DEV, flags=flags)
+    try:
+        for t in range(5):
+            std = wl.worker_std(t)
+            for j in range(K):
+                u = rng.random()
+                if u < 0.15:
+                    std[j] *= 30.0
+                elif u < 0.2:
+                    std[j] *= 1000.0
+            run.round(t, std=std, verbose=False)
+    except NearTie as e:
+        pytest.skip(str(e))
+    finally:
+        run.close()
