@@ -532,7 +532,7 @@ def main(argv=None) -> int:
             wl.fill_replicas(th.to(dev) if args.host_state else th, reps, u, t, args.seed, std=std)
         timed = t >= args.warmup
         if timed and t == args.warmup and not args.no_cpu_baseline:
-            for u in range(min(3, wl.num_units)):
+            for u in range(min(6, wl.num_units)):  # ~14 s of oracle time at the 1B shape
                 th, b, reps = units[u]
                 hb = [r.view(torch.int16).cpu().numpy().view(np.uint16) if r.dtype == torch.bfloat16
                       else r.cpu().numpy() for r in reps]
