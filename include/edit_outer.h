@@ -32,7 +32,8 @@
  * owns the handle, the EMA state, its scratch memory and its events.
  * Every function returns an edit_status_t; nothing is thrown across the ABI.
  * On failure, edit_outer_last_error() returns a message for the calling
- * thread.
+ * thread.  A handle is used from one host thread at a time (calls on
+ * different handles may come from different threads).
  */
 #ifndef EDIT_OUTER_H
 #define EDIT_OUTER_H
