@@ -214,9 +214,11 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
     K, R = wl.num_workers, wl.replica_bytes
     sizes = sorted(set(wl.layer_numel))
     groups, regs = {}, {}
+    spans = []  # (start, end, kind) of every dispatch, for the gaps between kernels
     with open(os.path.join(out_dir, f"prof_trace_{tag}", f"{tag}_kernel_trace.csv")) as f:
         for row in csv.DictReader(f):
             kind = _kernel_kind(row["Kernel_Name"])
+            spans.append((int(row["Start_Timestamp"]), int(row["End_Timestamp"]), kind))
             if not kind or kind == "copy_kernel":
                 continue
             grid = int(row.get("Grid_Size") or row.get("Grid_Size_X"))
@@ -255,6 +257,18 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
         gbps = f"{b / (avg * 1e-9) / 1e9:.1f}" if b else "-"
         lines.append(f"| {kind} | {grid} | {n if n else '-'} | {len(d)} | {avg / 1e3:.1f} | "
                      f"{min(d) / 1e3:.1f} | {max(d) / 1e3:.1f} | {b if b else '-'} | {gbps} |")
+    # idle time between consecutive dispatches that are both steps of the
+    # method (the stream's dependency latency; torch and copy kernels excluded)
+    spans.sort()
+    ours = {"pass1_gram_kernel", "pass1_gram_mfma_kernel", "decide_kernel", "pass2_update_kernel",
+            "fused_mean_kernel", "fused_finish_kernel"}
+    gaps = sorted(b[0] - a[1] for a, b in zip(spans, spans[1:]) if a[2] in ours and b[2] in ours)
+    if gaps:
+        med = gaps[len(gaps) // 2]
+        lines += ["", f"Gap between consecutive dispatches of the method's kernels (end of one to start "
+                  f"of the next, same stream): median {med / 1e3:.2f} us, 10th percentile "
+                  f"{gaps[len(gaps) // 10] / 1e3:.2f} us, 90th {gaps[9 * len(gaps) // 10] / 1e3:.2f} us "
+                  f"over {len(gaps)} pairs."]
     lines += ["", "Registers per lane (VGPR, AGPR) and LDS bytes per block, from the same trace:", ""]
     for kind, (v, a, l) in sorted(regs.items()):
         lines.append(f"- {kind}: {v} VGPR, {a} AGPR, {l} B LDS")
