@@ -618,7 +618,7 @@ def main(argv=None) -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f64",  # the arithmetic type; theta and b are stored fp32, replicas per config
         "data": "synthetic",
         "config": {
             "workload": f"{wl.name}: {wl.description}",
