@@ -182,7 +182,7 @@ def _profile_cmds(variant: str) -> dict:
     return {
         "tag": tag, "suffix": sfx,
         "trace": f"rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace{sfx} -o {tag} -- "
-                 f"python bench.py --steps 20 --warmup 10 --no-cpu-baseline{flag}",
+                 f"python bench.py{flag}",
         "fetch": f"rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/prof_fetch{sfx} -o {tag} -- "
                  f"python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0{flag}",
         "write": f"rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/prof_write{sfx} -o {tag} -- "
@@ -328,9 +328,10 @@ def summarize_profiles(out_dir: str, bench_json: str, variant: str = "two-pass")
     if dominant in stats and rl:
         ours = rl["avg_launch_ms"] * 1e3
         prof = stats[dominant]["AverageNs"] / 1e3
-        lines += ["", f"bench.py's own HIP-event average for {dominant} (sampled units, same "
-                  f"workload, default run{' with --one-pass' if one else ''}): {ours:.1f} us; "
-                  f"rocprofv3: {prof:.1f} us ({100 * (ours - prof) / prof:+.1f}%)."]
+        lines += ["", f"bench.py's own HIP-event average for {dominant} in the traced run "
+                  f"(sampled units, its JSON line's roofline.avg_launch_ms): {ours:.1f} us; "
+                  f"rocprofv3 over all launches of the same run: {prof:.1f} us "
+                  f"({100 * (ours - prof) / prof:+.1f}%)."]
     with open(os.path.join(prof_dir, f"{name}_kernel_trace_stats.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
