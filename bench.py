@@ -17,9 +17,7 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
-import math
 import os
-import statistics
 import sys
 import time
 

@@ -10,7 +10,6 @@ under its new index.
 """
 import dataclasses
 
-import numpy as np
 import pytest
 
 from parity import NearTie, ParityRun

@@ -14,7 +14,7 @@ import torch
 
 from oracle import OracleConfig, OracleUnit
 from parity import assert_tensor_close, compare_decision, host_bits
-from paper_2412_07210_amd import ONE_PASS, EditOuter, EditOuterError, OuterConfig, synth
+from paper_2412_07210_amd import ONE_PASS, EditOuter, OuterConfig, synth
 
 pytestmark = pytest.mark.gpu
 

@@ -11,8 +11,8 @@ import numpy as np
 import pytest
 import torch
 
-from parity import NearTie, ParityRun, host_bits
-from paper_2412_07210_amd import AE, GC, WA, EditOuter, EditOuterError, OuterConfig
+from parity import NearTie, ParityRun
+from paper_2412_07210_amd import EditOuter, EditOuterError, OuterConfig
 from paper_2412_07210_amd import synth
 
 pytestmark = pytest.mark.gpu
