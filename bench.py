@@ -267,9 +267,10 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
                   f"of the next, same stream): median {med / 1e3:.2f} us, 10th percentile "
                   f"{gaps[len(gaps) // 10] / 1e3:.2f} us, 90th {gaps[9 * len(gaps) // 10] / 1e3:.2f} us "
                   f"over {len(gaps)} pairs."]
-    lines += ["", "Registers per lane (VGPR, AGPR) and LDS bytes per block, from the same trace:", ""]
+    lines += ["", "The trace's VGPR_Count, Accum_VGPR_Count and LDS bytes per block (VGPR_Count reads "
+              "half the compiler's per-lane VGPR figure on this ROCm, e.g. 60 for a 119-VGPR kernel):", ""]
     for kind, (v, a, l) in sorted(regs.items()):
-        lines.append(f"- {kind}: {v} VGPR, {a} AGPR, {l} B LDS")
+        lines.append(f"- {kind}: VGPR_Count {v}, Accum_VGPR_Count {a}, {l} B LDS")
     text = "\n".join(lines) + "\n"
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
     with open(os.path.join(ROOT, "profiles", f"{tag}_kernel_trace_by_unit.md"), "w") as f:

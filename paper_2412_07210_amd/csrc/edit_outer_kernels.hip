@@ -28,7 +28,7 @@
 // vectors (the loads of trip t+1 are in flight while trip t is computed), so
 // the fp64 work hides under the memory latency even at 2 waves per SIMD.
 // Above K = 8 the Gram is a rank-n update on the fp64 matrix cores
-// (v_mfma_f64_16x16x4f64), which the VALU could not hold in registers.
+// (v_mfma_f64_4x4x4f64 tiles), which the VALU could not hold in registers.
 // Pass 2, which writes as much as it reads, instead gives each thread one
 // vector and lets the block dispatcher order the traffic (see there).
 //
@@ -453,72 +453,117 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_kernel(const fl
 
 // Pass 1 for 8 < K <= 16: the Gram matrix sum_i d_i d_i^T over the unit's
 // elements is a rank-n update, and with K(K+1)/2 = 136 fp64 sums per lane a
-// VALU version runs out of registers.  v_mfma_f64_16x16x4f64 keeps the whole
-// 16x16 Gram in 4 fp64 registers per lane: lane l holds worker l % 16's
-// pseudo gradient at vector slot l / 16, which is at once the A operand
-// (A[w][s], lane w + 16s) and the B operand (B[s][w], lane w + 16s), so each
-// instruction adds the outer products of 4 elements of all 16 workers.  The
-// result D[i][j] sits in lane j + 16 * (i % 4), register i / 4.  Lanes of
-// workers >= K feed zeros.
-typedef double f64x4 __attribute__((ext_vector_type(4)));
+// VALU version runs out of registers.  It runs on the fp64 matrix cores as
+// v_mfma_f64_4x4x4f64, four independent 4x4x4 products per wave instruction
+// (blocks b = 0..3).  The workers form G = ceil(K/4) groups of four and the
+// Gram matrix 4x4 tiles (I, J); only the G(G+1)/2 tiles with I <= J are
+// formed (10 of 16 at K = 16): 160 products per element where the 16x16x4
+// instruction forms all 256, and this one also sustains a higher share of
+// the fp64 matrix peak.  On gfx950 the fp64 matrix work and the fp64
+// vector work of the deltas (widening, subtracting theta) do not overlap,
+// so the pass is bound by their sum rather than by HBM.
+//
+// Operand layout of the instruction on gfx950 (checked with a one-hot
+// probe): lane l holds A[i][k] and B[k][j] of block b with i = j = l % 4,
+// b = (l / 4) % 4, k = l / 16, and the result D[i][j] of block b sits in
+// lane j + 4b + 16i.  So the four lanes of a quad q = l / 4 share (b, k):
+// they take one element, lane c = l % 4 holding the pseudo gradients of
+// workers c, c+4, c+8, c+12 of it, and for tile (I, J) a lane passes its
+// group-I value as A and its group-J value as B.  Each instruction adds the
+// products of 16 elements (one per quad) into the tile, block b summing the
+// quads b, b+4, b+8, b+12; the blocks are added at the end.
 
-// Worker w's replica at vector v, and theta element v*VE + w for lanes w < VE
-// (the 16 lanes of a slot then share theta by shuffles rather than each
-// loading the same 32 bytes).  Zero past the last full vector.
-template <bool BF16, bool NT>
-__device__ __forceinline__ void load_mfma(const float* theta, const void* rep, bool active, int w,
-                                          int64_t v, int64_t nvec, u32x4& raw, float& th) {
-  constexpr int VE = Vec<BF16>::VE;
-  raw = u32x4{0u, 0u, 0u, 0u};
-  th = 0.f;
-  if (v < nvec) {
-    if (w < VE) {
-      if constexpr (NT)
-        th = __builtin_nontemporal_load(theta + v * VE + w);
-      else
-        th = theta[v * VE + w];
-    }
-    if (active) raw = ld16<NT>(reinterpret_cast<const u32x4*>(rep) + v);
+// Vector slots per lane per loop trip of the matrix-core pass (two, or
+// loads two trips ahead, measured no faster and need 512-thread blocks).
+constexpr int kMfmaSlots = 1;
+
+template <int K>
+struct Tiles4 {
+  static constexpr int G = (K + 3) / 4;      // worker groups of four
+  static constexpr int T = G * (G + 1) / 2;  // tiles (I, J), I <= J
+};
+
+// Lane src's value within each quad of four lanes (DPP quad permutation).
+__device__ __forceinline__ float quad_bcast(float x, int src) {
+  const int xi = __float_as_int(x);
+  int r;
+  switch (src) {
+    case 0:
+      r = __builtin_amdgcn_mov_dpp(xi, 0x00, 0xf, 0xf, false);
+      break;
+    case 1:
+      r = __builtin_amdgcn_mov_dpp(xi, 0x55, 0xf, 0xf, false);
+      break;
+    case 2:
+      r = __builtin_amdgcn_mov_dpp(xi, 0xaa, 0xf, 0xf, false);
+      break;
+    default:
+      r = __builtin_amdgcn_mov_dpp(xi, 0xff, 0xf, 0xf, false);
+      break;
   }
+  return __int_as_float(r);
 }
 
-// The ragged tail (n - nvec*VE < VE elements), element by element, in slot 0.
-template <bool BF16>
-__device__ __forceinline__ void load_mfma_tail(const float* theta, const void* rep, bool active,
-                                               int w, int slot, int64_t nvec, int64_t n,
-                                               u32x4& raw, float& th) {
+// One vector slot of a quad: lane c's VE/4 theta values (elements
+// c*VE/4 ... of the vector) and its groups' replica vectors.
+template <int G, bool BF16>
+struct Quad4 {
+  u32x4 raw[G];
+  float th[Vec<BF16>::VE / 4];
+};
+
+template <int G, bool BF16, bool NT>
+__device__ __forceinline__ void load_quad4(const float* theta, const void* const (&rep)[G],
+                                           const bool (&act)[G], int c, int64_t v, int64_t nvec,
+                                           Quad4<G, BF16>& q) {
   constexpr int VE = Vec<BF16>::VE;
-  raw = u32x4{0u, 0u, 0u, 0u};
-  th = 0.f;
-  if (slot != 0) return;
-  if (w < VE && nvec * VE + w < n) th = theta[nvec * VE + w];
-  if (!active) return;
 #pragma unroll
-  for (int e = 0; e < VE; ++e) {
-    const int64_t i = nvec * VE + e;
-    if (i < n) {
-      if constexpr (BF16) {
-        const uint32_t h = reinterpret_cast<const uint16_t*>(rep)[i];
-        raw[e >> 1] |= (e & 1) ? (h << 16) : h;
-      } else {
-        raw[e] = __float_as_uint(reinterpret_cast<const float*>(rep)[i]);
-      }
+  for (int g = 0; g < G; ++g) q.raw[g] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int t = 0; t < VE / 4; ++t) q.th[t] = 0.f;
+  if (v < nvec) {
+    const float* tp = theta + v * VE + c * (VE / 4);
+    if constexpr (BF16) {
+      const float2_t t2 = NT ? __builtin_nontemporal_load(reinterpret_cast<const float2_t*>(tp))
+                             : *reinterpret_cast<const float2_t*>(tp);
+      q.th[0] = t2[0];
+      q.th[1] = t2[1];
+    } else {
+      q.th[0] = NT ? __builtin_nontemporal_load(tp) : *tp;
     }
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      if (act[g]) q.raw[g] = ld16<NT>(reinterpret_cast<const u32x4*>(rep[g]) + v);
   }
 }
 
-template <bool BF16>
-__device__ __forceinline__ void gram_mfma(f64x4& acc0, f64x4& acc1, const u32x4& raw, float th_lane,
-                                          int lane, bool active) {
+// The Gram tiles of one vector slot: theta element e comes from lane
+// e / (VE/4) of the quad.
+template <int K, bool BF16>
+__device__ __forceinline__ void gram_quad4(double (&acc)[Tiles4<K>::T], const u32x4 (&raw)[Tiles4<K>::G],
+                                           const float (&th)[Vec<BF16>::VE], const bool (&act)[Tiles4<K>::G]) {
+  constexpr int G = Tiles4<K>::G;
 #pragma unroll
   for (int e = 0; e < Vec<BF16>::VE; ++e) {
-    const float th = __shfl(th_lane, (lane & 48) + e, 64);  // every lane takes part
-    const double d = active ? delta64<BF16>(raw, e, th) : 0.0;
-    if (e & 1)
-      acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(d, d, acc1, 0, 0, 0);
-    else
-      acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(d, d, acc0, 0, 0, 0);
+    double d[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) d[g] = act[g] ? delta64<BF16>(raw[g], e, th[e]) : 0.0;
+    int t = 0;
+#pragma unroll
+    for (int I = 0; I < G; ++I)
+#pragma unroll
+      for (int J = I; J < G; ++J, ++t) acc[t] = __builtin_amdgcn_mfma_f64_4x4x4f64(d[I], d[J], acc[t], 0, 0, 0);
   }
+}
+
+template <int K, bool BF16>
+__device__ __forceinline__ void gram_quad4_bcast(double (&acc)[Tiles4<K>::T], const Quad4<Tiles4<K>::G, BF16>& q,
+                                                 const bool (&act)[Tiles4<K>::G]) {
+  constexpr int VE = Vec<BF16>::VE;
+  float th[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) th[e] = quad_bcast(q.th[e % (VE / 4)], e / (VE / 4));
+  gram_quad4<K, BF16>(acc, q.raw, th, act);
 }
 
 template <int K, bool BF16, bool NT>
@@ -538,63 +583,103 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_mfma_kernel(con
   const int rows = static_cast<int>(gridDim.x) - first;
   constexpr int NP = K * (K + 1) / 2;
   constexpr int VE = Vec<BF16>::VE;
+  constexpr int G = Tiles4<K>::G;
+  constexpr int T = Tiles4<K>::T;
   constexpr int kWaves = pass1_threads<K>() / 64;
-  // Vectors per lane per group (a group is 4*V consecutive vectors of every
-  // worker).  A wave instruction reads 64 bytes of each of 16 workers, half a
-  // cache line; with cached loads the other half is an L2 hit, where
-  // non-temporal loads fetched it again (measured at K = 16, 51.4M elements:
-  // 380 us for the loads alone cached, 480 us non-temporal).  The kernel as a
-  // whole is bound by the fp64 MFMA rate instead: 256 products per element
-  // (the symmetric half is computed too) at the ~48 TFLOP/s this instruction
-  // sustains here, about 550 us for that unit.
-  constexpr int V = 4;
+  // Vector slots per lane per group; a group is 16*V consecutive vectors of
+  // every worker, and one wave load instruction reads 256 contiguous bytes
+  // of each of four replicas.
+  constexpr int V = kMfmaSlots;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int w = lane & 15;
-  const int slot = lane >> 4;
-  const bool active = w < K;
-  const void* rep = reps.p[0];
+  const int c = lane & 3;
+  const int quad = lane >> 2;
+  const void* rep[G];
+  bool act[G];
 #pragma unroll
-  for (int j = 1; j < K; ++j) rep = (w == j) ? reps.p[j] : rep;
+  for (int g = 0; g < G; ++g) {
+    const int w = 4 * g + c;
+    act[g] = w < K;
+    rep[g] = reps.p[4 * g];
+#pragma unroll
+    for (int j = 4 * g + 1; j < 4 * g + 4 && j < K; ++j) rep[g] = (w == j) ? reps.p[j] : rep[g];
+  }
 
-  const int64_t groups = (nvec + 4 * V - 1) / (4 * V);
+  const int64_t groups = (nvec + 16 * V - 1) / (16 * V);
   const int64_t wave_stride = static_cast<int64_t>(rows) * kWaves;
-  auto load = [&](int64_t g, u32x4 (&raw)[V], float (&th)[V]) {
+  auto load = [&](int64_t g, Quad4<G, BF16> (&q)[V]) {
 #pragma unroll
-    for (int u = 0; u < V; ++u)
-      load_mfma<BF16, NT>(theta, rep, active, w, 4 * V * g + 4 * u + slot, nvec, raw[u], th[u]);
+    for (int u = 0; u < V; ++u) load_quad4<G, BF16, NT>(theta, rep, act, c, 16 * V * g + 16 * u + quad, nvec, q[u]);
   };
-  auto accumulate = [&](f64x4& a0, f64x4& a1, const u32x4 (&raw)[V], const float (&th)[V]) {
+  auto accumulate = [&](double (&acc)[T], const Quad4<G, BF16> (&q)[V]) {
 #pragma unroll
-    for (int u = 0; u < V; ++u) gram_mfma<BF16>(a0, a1, raw[u], th[u], lane, active);
+    for (int u = 0; u < V; ++u) gram_quad4_bcast<K, BF16>(acc, q[u], act);
   };
+  double acc[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) acc[t] = 0.0;
   int64_t g = static_cast<int64_t>(b) * kWaves + wave;
-  f64x4 acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
-  float thA[V], thB[V];
-  u32x4 rA[V], rB[V];
-  load(g, rA, thA);
-  while (g < groups) {  // double-buffered like the VALU pass
-    load(g + wave_stride, rB, thB);
-    accumulate(acc0, acc1, rA, thA);
+  Quad4<G, BF16> qA[V], qB[V];
+  load(g, qA);
+  while (g < groups) {  // double-buffered like the VALU pass; wave-uniform
+    load(g + wave_stride, qB);
+    accumulate(acc, qA);
     g += wave_stride;
     if (g >= groups) break;
-    load(g + wave_stride, rA, thA);
-    accumulate(acc0, acc1, rB, thB);
+    load(g + wave_stride, qA);
+    accumulate(acc, qB);
     g += wave_stride;
   }
-  if (b == 0 && wave == 0 && n > nvec * VE) {  // wave-uniform: MFMA needs all lanes
-    u32x4 raw;
-    float th;
-    load_mfma_tail<BF16>(theta, rep, active, w, slot, nvec, n, raw, th);
-    gram_mfma<BF16>(acc0, acc1, raw, th, lane, active);
-  }
-  const f64x4 acc = acc0 + acc1;
-
-  // Block reduction: each wave's 16x16 Gram to LDS, then the four waves in
-  // order for each upper-triangle pair.
-  __shared__ double gsh[kWaves][16][16];
+  // Ragged tail (fewer than VE elements past the last full vector): quad 0
+  // of row 0's first wave, element by element.  Wave-uniform, as the matrix
+  // instruction needs every lane.
+  if (b == 0 && wave == 0 && n > nvec * VE) {
+    u32x4 raw[G];
+    float th[VE];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) gsh[wave][slot + 4 * r][w] = acc[r];
+    for (int g = 0; g < G; ++g) raw[g] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      const int64_t i = nvec * VE + e;
+      th[e] = (quad == 0 && i < n) ? theta[i] : 0.f;
+    }
+    if (quad == 0) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        if (!act[g]) continue;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const int64_t i = nvec * VE + e;
+          if (i < n) {
+            if constexpr (BF16) {
+              const uint32_t h = reinterpret_cast<const uint16_t*>(rep[g])[i];
+              raw[g][e >> 1] |= (e & 1) ? (h << 16) : h;
+            } else {
+              raw[g][e] = __float_as_uint(reinterpret_cast<const float*>(rep[g])[i]);
+            }
+          }
+        }
+      }
+    }
+    gram_quad4<K, BF16>(acc, raw, th, act);
+  }
+
+  // Block reduction: add the four instruction blocks (lanes l, l^4, l^8,
+  // l^12), write each wave's tiles to LDS, then the waves in order for each
+  // upper-triangle pair.
+  __shared__ double gsh[kWaves][16][16];
+  {
+    int t = 0;
+#pragma unroll
+    for (int I = 0; I < G; ++I)
+#pragma unroll
+      for (int J = I; J < G; ++J, ++t) {
+        double x = acc[t];
+        x += __shfl_xor(x, 4, 64);
+        x += __shfl_xor(x, 8, 64);
+        if ((quad & 3) == 0) gsh[wave][4 * I + (lane >> 4)][4 * J + c] = x;
+      }
+  }
   __syncthreads();
   for (int p = threadIdx.x; p < NP; p += pass1_threads<K>()) {
     int j = 0, left = p;
@@ -609,7 +694,6 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_mfma_kernel(con
     partials[static_cast<int64_t>(p) * rows + b] = s;
   }
 }
-
 // ---------------------------------------------------------------- decide
 
 template <int K>
