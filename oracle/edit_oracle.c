@@ -13,6 +13,9 @@
  *   OuterOpt = Nesterov momentum             Sec. 4.1 (after DiLoCo)
  *   write-back to every worker               Algorithm 2
  *
+ * oracle_decide_gram takes the same decision from a given Gram matrix of the
+ * pseudo gradients (norms from its diagonal, Gbar^2 = w^T Gram w).
+ *
  * Readings taken where the paper is silent (each listed in the design notes):
  *   - OuterOpt consumes the outer gradient g = -Delta_hat, in the form of
  *     SGD with Nesterov momentum: b' = rho*b + g; theta' = theta - nu*(g + rho*b').
@@ -23,6 +26,8 @@
  *     unmasked norm (identical to Eq. 2 unless every exp(-G) underflows).
  *   - A rollback leaves theta, the momentum and the EMA state unchanged and
  *     only resets the replicas; the round counter still advances.
+ *   - A quadratic form w^T Gram w that rounding takes below zero is a squared
+ *     norm and counts as 0.
  */
 #include "edit_oracle.h"
 
@@ -126,41 +131,33 @@ static void write_back_all(void *const *replicas, int K, int is_bf16, int64_t i,
   }
 }
 
-int oracle_step(const oracle_cfg_t *cfg, int K, int64_t n, int replica_is_bf16,
-                float *theta, float *momentum, void *const *replicas,
-                oracle_ema_t *ema, oracle_record_t *rec) {
-  if (!cfg || !ema || K < 1 || K > ORACLE_MAX_K || n < 0) return -1;
-  if (n > 0 && (!theta || !momentum || !replicas)) return -1;
-  for (int j = 0; j < K && n > 0; ++j)
-    if (!replicas[j]) return -1;
+/* Eq. 4: beta = min(phi / (Gbar + eps), 1) with the clip on, else 1. */
+static double clip_coefficient(const oracle_cfg_t *cfg, double gbar) {
+  if (!(cfg->flags & ORACLE_GC)) return 1.0;
+  return fmin(cfg->clip_threshold / (gbar + cfg->clip_eps), 1.0);
+}
 
+/* The decision from the norms G_j, shared by the step and by the decision
+ * on a given Gram matrix: anomaly elimination (Sec. 3.2; a flagged worker's
+ * norm counts as infinite, so it drops out of Eq. 2 and its EMA update is
+ * skipped), the EMA update of Eq. 1, and the weights of Eq. 2 (1/|U| each
+ * without weighted averaging).  Fills the record's norms, mask, margins and
+ * weights; returns the number of unflagged workers (0: rollback). */
+static int decide_weights(const oracle_cfg_t *cfg, int K, const double *G, oracle_ema_t *ema,
+                          oracle_record_t *r, int *anomalous, double *w) {
   const int ae = (cfg->flags & ORACLE_AE) != 0;
   const int wa = (cfg->flags & ORACLE_WA) != 0;
-  const int gc = (cfg->flags & ORACLE_GC) != 0;
-  const int bf16 = replica_is_bf16 != 0;
+  for (int j = 0; j < K; ++j) r->norm[j] = G[j];
 
-  oracle_record_t r;
-  memset(&r, 0, sizeof r);
-
-  /* Pseudo gradient norms. */
-  double G[ORACLE_MAX_K];
-  for (int j = 0; j < K; ++j) {
-    G[j] = pseudo_gradient_norm(replicas[j], bf16, theta, n);
-    r.norm[j] = G[j];
-  }
-
-  /* Anomaly elimination: a flagged worker's norm becomes infinite, so it
-   * drops out of Eq. 2 and its EMA update is skipped. */
-  int anomalous[ORACLE_MAX_K];
   const int z_test = ae && ema->round >= cfg->warmup_rounds;
-  r.z_tested = z_test;
+  r->z_tested = z_test;
   for (int j = 0; j < K; ++j) {
-    r.margin[j] = INFINITY;
+    r->margin[j] = INFINITY;
     anomalous[j] = !isfinite(G[j]);
     if (z_test && !anomalous[j])
       anomalous[j] = is_anomaly(G[j], ema->mu[j], ema->sigma[j], cfg->z_threshold,
-                                &r.margin[j]);
-    r.anomalous[j] = (uint8_t)anomalous[j];
+                                &r->margin[j]);
+    r->anomalous[j] = (uint8_t)anomalous[j];
   }
   if (ae)
     for (int j = 0; j < K; ++j)
@@ -168,18 +165,8 @@ int oracle_step(const oracle_cfg_t *cfg, int K, int64_t n, int replica_is_bf16,
 
   int n_ok = 0;
   for (int j = 0; j < K; ++j) n_ok += !anomalous[j];
+  if (n_ok == 0) return 0;
 
-  if (n_ok == 0) {
-    /* Rollback: every worker returns to the last synchronized theta_t. */
-    for (int64_t i = 0; i < n; ++i) write_back_all(replicas, K, bf16, i, theta[i]);
-    r.rolled_back = 1;
-    ema->round += 1;
-    if (rec) *rec = r;
-    return 0;
-  }
-
-  /* Weighted averaging, Eq. 2. */
-  double w[ORACLE_MAX_K];
   if (wa) {
     double g0 = INFINITY;
     for (int j = 0; j < K; ++j)
@@ -193,7 +180,40 @@ int oracle_step(const oracle_cfg_t *cfg, int K, int64_t n, int replica_is_bf16,
   } else {
     for (int j = 0; j < K; ++j) w[j] = anomalous[j] ? 0.0 : 1.0 / (double)n_ok;
   }
-  for (int j = 0; j < K; ++j) r.weight[j] = w[j];
+  for (int j = 0; j < K; ++j) r->weight[j] = w[j];
+  return n_ok;
+}
+
+int oracle_step(const oracle_cfg_t *cfg, int K, int64_t n, int replica_is_bf16,
+                float *theta, float *momentum, void *const *replicas,
+                oracle_ema_t *ema, oracle_record_t *rec) {
+  if (!cfg || !ema || K < 1 || K > ORACLE_MAX_K || n < 0) return -1;
+  if (n > 0 && (!theta || !momentum || !replicas)) return -1;
+  for (int j = 0; j < K && n > 0; ++j)
+    if (!replicas[j]) return -1;
+
+  const int bf16 = replica_is_bf16 != 0;
+
+  oracle_record_t r;
+  memset(&r, 0, sizeof r);
+
+  /* Pseudo gradient norms. */
+  double G[ORACLE_MAX_K];
+  for (int j = 0; j < K; ++j) G[j] = pseudo_gradient_norm(replicas[j], bf16, theta, n);
+
+  /* Anomaly elimination, the EMA update and the weights of Eq. 2. */
+  int anomalous[ORACLE_MAX_K];
+  double w[ORACLE_MAX_K];
+  const int n_ok = decide_weights(cfg, K, G, ema, &r, anomalous, w);
+
+  if (n_ok == 0) {
+    /* Rollback: every worker returns to the last synchronized theta_t. */
+    for (int64_t i = 0; i < n; ++i) write_back_all(replicas, K, bf16, i, theta[i]);
+    r.rolled_back = 1;
+    ema->round += 1;
+    if (rec) *rec = r;
+    return 0;
+  }
 
   /* Eq. 3: Delta_bar = sum_j w_j Delta_j, materialised. */
   double *dbar = NULL;
@@ -212,7 +232,7 @@ int oracle_step(const oracle_cfg_t *cfg, int K, int64_t n, int replica_is_bf16,
   double ss = 0.0;
   for (int64_t i = 0; i < n; ++i) ss += dbar[i] * dbar[i];
   const double gbar = sqrt(ss);
-  const double beta = gc ? fmin(cfg->clip_threshold / (gbar + cfg->clip_eps), 1.0) : 1.0;
+  const double beta = clip_coefficient(cfg, gbar);
   r.synced_norm = gbar;
   r.clip_coef = beta;
 
@@ -229,6 +249,54 @@ int oracle_step(const oracle_cfg_t *cfg, int K, int64_t n, int replica_is_bf16,
     write_back_all(replicas, K, bf16, i, theta[i]);
   }
   free(dbar);
+
+  ema->round += 1;
+  if (rec) *rec = r;
+  return 0;
+}
+
+/* ------------------------------------------------ decision from a Gram */
+
+int oracle_decide_gram(const oracle_cfg_t *cfg, int K, const double *gram, oracle_ema_t *ema,
+                       oracle_record_t *rec) {
+  if (!cfg || !ema || !gram || K < 1 || K > ORACLE_MAX_K) return -1;
+
+  /* Entry (j, k), j <= k, of the row-major upper triangle. */
+#define GRAM_AT(j, k) gram[(j) * K - ((j) * ((j) - 1)) / 2 + ((k) - (j))]
+
+  oracle_record_t r;
+  memset(&r, 0, sizeof r);
+
+  /* G_j = ||Delta_j||_2 = sqrt(<Delta_j, Delta_j>). */
+  double G[ORACLE_MAX_K];
+  for (int j = 0; j < K; ++j) G[j] = sqrt(GRAM_AT(j, j));
+
+  int anomalous[ORACLE_MAX_K];
+  double w[ORACLE_MAX_K];
+  const int n_ok = decide_weights(cfg, K, G, ema, &r, anomalous, w);
+  if (n_ok == 0) {
+    r.rolled_back = 1;
+    ema->round += 1;
+    if (rec) *rec = r;
+    return 0;
+  }
+
+  /* Eq. 3-4: ||sum_j w_j Delta_j||^2 = sum_j sum_k w_j w_k <Delta_j, Delta_k>
+   * over the unflagged workers (a flagged worker's entries may be
+   * non-finite and have weight 0).  The sum is a squared norm, so a value
+   * that rounding took below zero counts as zero. */
+  double q = 0.0;
+  for (int j = 0; j < K; ++j) {
+    if (anomalous[j]) continue;
+    for (int k = 0; k < K; ++k) {
+      if (anomalous[k]) continue;
+      q += w[j] * w[k] * (j <= k ? GRAM_AT(j, k) : GRAM_AT(k, j));
+    }
+  }
+#undef GRAM_AT
+  const double gbar = sqrt(q > 0.0 ? q : 0.0);
+  r.synced_norm = gbar;
+  r.clip_coef = clip_coefficient(cfg, gbar);
 
   ema->round += 1;
   if (rec) *rec = r;

@@ -80,6 +80,21 @@ int oracle_step(const oracle_cfg_t *cfg, int K, int64_t n, int replica_is_bf16,
                 float *theta, float *momentum, void *const *replicas,
                 oracle_ema_t *ema, oracle_record_t *rec);
 
+/*
+ * The decision of one step taken from a given Gram matrix of the K pseudo
+ * gradients, Gram_jk = <Delta_j, Delta_k> (Sec. 3.2, Eq. 1-4), without the
+ * elementwise update: G_j = sqrt(Gram_jj); the mask, EMA update and weights
+ * exactly as in oracle_step; Gbar^2 = sum_jk w_j w_k Gram_jk over the
+ * unflagged workers (taken as 0 if rounding makes it negative); beta.
+ *   gram  [K(K+1)/2] fp64, the upper triangle row by row:
+ *         (0,0), (0,1), ..., (0,K-1), (1,1), ..., (K-1,K-1)
+ *   ema   in/out EMA state and round counter of the module
+ *   rec   out: the decision record (may be NULL)
+ * Returns 0, or -1 for bad arguments.
+ */
+int oracle_decide_gram(const oracle_cfg_t *cfg, int K, const double *gram, oracle_ema_t *ema,
+                       oracle_record_t *rec);
+
 /* Round-to-nearest-even of an fp32 value to bfloat16 (bit pattern). */
 uint16_t oracle_f32_to_bf16(float x);
 

@@ -75,6 +75,11 @@ def _lib():
             ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p),
             ctypes.POINTER(_Ema), ctypes.POINTER(_Record),
         ]
+        lib.oracle_decide_gram.restype = ctypes.c_int
+        lib.oracle_decide_gram.argtypes = [
+            ctypes.POINTER(_Cfg), ctypes.c_int, ctypes.c_void_p, ctypes.POINTER(_Ema),
+            ctypes.POINTER(_Record),
+        ]
         lib.oracle_f32_to_bf16.restype = ctypes.c_uint16
         lib.oracle_f32_to_bf16.argtypes = [ctypes.c_float]
         lib.oracle_bf16_to_f32.restype = ctypes.c_float
@@ -152,6 +157,25 @@ class OracleUnit:
                                 ctypes.byref(self._ema), ctypes.byref(rec))
         if rc != 0:
             raise RuntimeError("oracle_step failed with %d" % rc)
+        return self._record(rec)
+
+    def decide_gram(self, gram: np.ndarray) -> dict:
+        """The decision of one step from a given Gram matrix of the pseudo
+        gradients (upper triangle row by row, fp64), advancing the EMA state
+        as step() does; no elementwise update."""
+        K = self.num_workers
+        g = np.ascontiguousarray(gram, dtype=np.float64)
+        if g.shape != (K * (K + 1) // 2,):
+            raise ValueError("expected the %d upper-triangle entries" % (K * (K + 1) // 2))
+        rec = _Record()
+        rc = _lib().oracle_decide_gram(ctypes.byref(self.config._c()), K, g.ctypes.data,
+                                       ctypes.byref(self._ema), ctypes.byref(rec))
+        if rc != 0:
+            raise RuntimeError("oracle_decide_gram failed with %d" % rc)
+        return self._record(rec)
+
+    def _record(self, rec: "_Record") -> dict:
+        K = self.num_workers
         return {
             "norm": np.array(rec.norm[:K]),
             "anomalous": np.array(rec.anomalous[:K], dtype=np.uint8),

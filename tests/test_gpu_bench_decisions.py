@@ -1,0 +1,94 @@
+"""The benchmark workload's decisions, every unit and every round, against the
+oracle's decision on the library's own Gram matrices.
+
+The 1B K = 8 bf16 workload (24 units of 51,384,320 elements) is stepped with
+edit_outer_step_round, the call the benchmark times, for the benchmark's
+100 rounds with its seeds (so these are the decisions of a default benchmark
+run): ten warm-up rounds of the EMA state (Sec. 3.2), then z-tested rounds in
+which the per-worker pseudo-gradient scales vary (so workers are also
+flagged on their own), with one worker x20 in rounds 19, 29, ..., 99.
+Before each round every unit's Gram matrix is exported with
+edit_outer_gram_layer, which reduces the same partial sums in the same order
+as the step, so it is the matrix the step decides on.  The oracle takes its decision from that matrix
+(oracle_decide_gram), carrying its own EMA state from round to round, and
+the library's record must agree: the mask exactly, the round counter,
+rollback and z-test flags, and the norms, weights, EMA state, Gbar and beta
+to 1e-13 relative.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import OracleConfig, OracleUnit
+from paper_2412_07210_amd import EditOuter, OuterConfig, synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+ROUNDS = 100  # the benchmark's default warm-up + timed rounds
+RTOL = 1e-13
+TIE = 1e-12  # z-test margins this close to a tie may round either way
+
+
+def _close(lib, ref, what):
+    lib = np.asarray(lib, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    ok = (lib == ref) | (np.abs(lib - ref) <= RTOL * np.abs(ref))
+    assert ok.all(), f"{what}: library {lib} oracle {ref}"
+
+
+def test_every_decision_of_the_1b_workload():
+    wl = synth.get("llama1b-k8-bf16")
+    K, L = wl.num_workers, wl.num_units
+    hyper = wl.hyper()
+    warm = hyper.pop("warmup_rounds")
+    lib = EditOuter(OuterConfig(num_workers=K, layer_numel=wl.layer_numel, replica_dtype=wl.replica_dtype,
+                                ema_warmup_rounds=warm, **hyper), DEV)
+    oracles = [OracleUnit(K, OracleConfig(**wl.hyper())) for _ in range(L)]
+    try:
+        units = []
+        for u in range(L):
+            th = wl.init_theta(u, DEV)
+            units.append((th, torch.zeros_like(th),
+                          [torch.empty(th.numel(), dtype=wl.torch_dtype, device=DEV) for _ in range(K)]))
+        grams = torch.empty(L, lib.num_pairs, dtype=torch.float64, device=DEV)
+        plan = lib.prepare_round(units)
+        masked = 0
+        for t in range(ROUNDS):
+            std = wl.worker_std(t)
+            for u, (th, _, reps) in enumerate(units):
+                wl.fill_replicas(th, reps, u, t, std=std)
+            for u, (th, _, reps) in enumerate(units):
+                lib.gram_layer(u, th, reps, gram=grams[u])
+            plan.run()
+            torch.cuda.synchronize(DEV)
+            g = grams.cpu().numpy()
+            boosted = wl.anomalies(t)
+            for u in range(L):
+                what = f"round {t} unit {u}"
+                rec = oracles[u].decide_gram(g[u])
+                st = lib.state_get(u)
+                mask_l = np.asarray(st.anomalous[:K], dtype=np.uint8)
+                mask_o = rec["anomalous"]
+                differ = mask_l != mask_o
+                if differ.any() and (rec["margin"][differ] < TIE).all():
+                    pytest.skip(f"{what}: z-test within rounding of a tie")
+                assert np.array_equal(mask_l, mask_o), f"{what}: mask library {mask_l} oracle {mask_o}"
+                assert st.round == rec["round"] == t + 1, what
+                assert int(st.rolled_back) == rec["rolled_back"], what
+                assert int(st.z_tested) == rec["z_tested"] == int(t >= warm), what
+                _close(st.norm[:K], rec["norm"], what + ": G")
+                _close(st.weight[:K], rec["weight"], what + ": w")
+                _close(st.ema_mean[:K], rec["mu"], what + ": mu")
+                _close(st.ema_std[:K], rec["sigma"], what + ": sigma")
+                if not rec["rolled_back"]:
+                    _close(st.synced_norm, rec["synced_norm"], what + ": Gbar")
+                    _close(st.clip_coef, rec["clip_coef"], what + ": beta")
+                for j in boosted:  # a x20 worker fails the z-test in every unit
+                    assert mask_o[j] == 1, f"{what}: boosted worker {j} not flagged"
+                masked += int(mask_o.sum())
+            print(f"  round {t}: {L} units agree, boosted {sorted(boosted)}, masked so far {masked}",
+                  flush=True)
+        assert masked > 9 * L  # the boosted rounds alone flag 9L workers
+    finally:
+        lib.close()

@@ -2,8 +2,9 @@
 
 A small C driver steps the oracle over edge sizes (n = 0, 1, 7, 8, 1000),
 K = 1..5 and 64, both replica types, all eight switch combinations, a
-rollback round and NaN/Inf inputs, with the sanitizers aborting on the first
-report.  Only host code is compiled here (gcc), nothing for a GPU.
+rollback round and NaN/Inf inputs, and takes the decision from exactly sized
+Gram arrays (same K and switches, NaN/Inf entries), with the sanitizers
+aborting on the first report.  Only host code is compiled here (gcc), nothing for a GPU.
 """
 import os
 import shutil
@@ -51,6 +52,23 @@ static int run(int K, int64_t n, int bf16, uint32_t flags, int poison) {
   return 0;
 }
 
+/* The decision from a Gram matrix, over an exactly sized heap array. */
+static int run_gram(int K, uint32_t flags, int poison) {
+  oracle_cfg_t cfg = {0.8, 0.85, 0.05, 1e-6, 0.02, 3.0, 2, flags};
+  oracle_ema_t ema = {{0}, {0}, 0};
+  oracle_record_t rec;
+  const int np = K * (K + 1) / 2;
+  double *gram = malloc(sizeof(double) * np);
+  for (int round = 0; round < 5; ++round) {
+    for (int p = 0; p < np; ++p) gram[p] = 1e-3 * (uni() - 0.25);
+    for (int j = 0, p = 0; j < K; p += K - j, ++j) gram[p] = (round == 4 ? 1e4 : 1.0) * 1e-2 * (1.0 + uni());
+    if (poison && K > 1) { gram[1] = NAN; gram[np - 1] = INFINITY; }
+    if (oracle_decide_gram(&cfg, K, gram, &ema, &rec) != 0) return 1;
+  }
+  free(gram);
+  return 0;
+}
+
 int main(void) {
   const int Ks[] = {1, 2, 3, 4, 5, 64};
   const int64_t ns[] = {0, 1, 7, 8, 1000};
@@ -63,12 +81,22 @@ int main(void) {
             if (run(Ks[k], ns[m], bf16, flags, poison)) { printf("step failed\n"); return 1; }
             ++runs;
           }
+  for (unsigned k = 0; k < sizeof Ks / sizeof Ks[0]; ++k)
+    for (uint32_t flags = 0; flags < 8; ++flags)
+      for (int poison = 0; poison < 2; ++poison) {
+        if (run_gram(Ks[k], flags, poison)) { printf("decision failed\n"); return 1; }
+        ++runs;
+      }
   /* bad arguments are refused, not dereferenced */
   oracle_cfg_t cfg = {0.8, 0.85, 10, 1e-6, 0.02, 3, 10, 7};
   oracle_ema_t ema = {{0}, {0}, 0};
   if (oracle_step(&cfg, 0, 4, 0, NULL, NULL, NULL, &ema, NULL) != -1) return 2;
   if (oracle_step(&cfg, 65, 4, 0, NULL, NULL, NULL, &ema, NULL) != -1) return 2;
   if (oracle_step(&cfg, 2, 4, 0, NULL, NULL, NULL, &ema, NULL) != -1) return 2;
+  double g[3] = {1, 0, 1};
+  if (oracle_decide_gram(&cfg, 2, NULL, &ema, NULL) != -1) return 2;
+  if (oracle_decide_gram(&cfg, 0, g, &ema, NULL) != -1) return 2;
+  if (oracle_decide_gram(&cfg, 65, g, &ema, NULL) != -1) return 2;
   printf("ok %d runs\n", runs);
   return 0;
 }
