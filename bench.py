@@ -396,6 +396,166 @@ def summarize_profiles(out_dir: str, bench_json: str, variant: str = "two-pass")
         f.write("\n")
     print(json.dumps(out))
 
+def run_sync_group(args, torch, np, wl, dev) -> int:
+    """One worker's share of a sync group whose K replicas sit on K GPUs
+    (rank `--sync-group-rank`): per unit, edit_group_norm (norm pass and the
+    worker's own z-test), edit_group_weights (the group decision) and
+    edit_group_apply (Delta_bar norm, clip, Nesterov, the own replica).  The
+    two collectives between them are not this GPU's kernels and are stood in
+    for on the device: the all-gather by a copy of the rank's own {G, flag}
+    pair into all K slots (so every worker counts as unflagged), the
+    all-reduce by nothing (the rank's own export serves as Delta_bar).  The
+    timed step is the rank's kernels for every unit; its bytes per element
+    are (4 + R + 4) for the norm pass, 4 for the Delta_bar pass and
+    12 + 8 + R for the update."""
+    from paper_2412_07210_amd import OuterConfig, SyncGroupWorker
+
+    K, R = wl.num_workers, wl.replica_bytes
+    rank = args.sync_group_rank
+    if not 0 <= rank < K:
+        print(json.dumps({"error": f"--sync-group-rank must be in 0..{K - 1}"}), flush=True)
+        return 2
+    hyper = wl.hyper()
+    warm = hyper.pop("warmup_rounds")
+    w = SyncGroupWorker(OuterConfig(num_workers=K, layer_numel=wl.layer_numel, replica_dtype=wl.replica_dtype,
+                                    ema_warmup_rounds=warm, **hyper), rank, dev)
+    log(f"sync-group worker {rank} of {K}: {wl.num_units} units of {wl.name}")
+    units = []
+    for u in range(wl.num_units):
+        th = wl.init_theta(u, dev, args.seed)
+        units.append(dict(th=th, b=torch.zeros_like(th), rep=torch.empty(th.numel(), dtype=wl.torch_dtype, device=dev),
+                          delta=torch.empty_like(th), pair=torch.empty(2, dtype=torch.float64, device=dev),
+                          gathered=torch.empty(K, 2, dtype=torch.float64, device=dev),
+                          w=torch.empty(1, dtype=torch.float64, device=dev)))
+
+    def step(u, d, ev=None):
+        if ev is not None:
+            ev[0].record()
+        w.norm(u, d["th"], d["rep"], d["delta"], d["pair"])
+        if ev is not None:
+            ev[1].record()
+        d["gathered"].copy_(d["pair"].expand(K, 2))  # stands in for the all-gather
+        w.weights(u, d["gathered"].view(-1), d["delta"], d["w"])
+        if ev is not None:
+            ev[2].record()
+        w.apply(u, d["delta"], d["th"], d["b"], d["rep"])  # the own export stands in for Delta_bar
+        if ev is not None:
+            ev[3].record()
+
+    every = max(1, args.profile_every) if args.profile_every > 0 else 0
+    step_ms, norm_ms, apply_ms = [], [], []
+    for t in range(args.warmup + args.steps):
+        for u, d in enumerate(units):
+            wl.fill_replicas(d["th"], [d["rep"]], u, t, args.seed)
+        torch.cuda.synchronize()
+        if t == 1:  # leave the warm-up: an EMA state that every later norm passes
+            for u, d in enumerate(units):
+                G = float(d["pair"][0])
+                w.state_set(u, G, 10.0 * G, warm)
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        evs = {u: [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+               for u in range(wl.num_units) if every and u % every == 0}
+        a.record()
+        for u, d in enumerate(units):
+            step(u, d, evs.get(u))
+        z.record()
+        torch.cuda.synchronize()
+        if t < args.warmup:
+            continue
+        step_ms.append(a.elapsed_time(z))
+        for u, ev in evs.items():
+            norm_ms.append(ev[0].elapsed_time(ev[1]))
+            apply_ms.append(ev[2].elapsed_time(ev[3]))
+    states = [w.state_get(u) for u in range(wl.num_units)]
+    w.close()
+    n_tot = sum(wl.layer_numel)
+    step_bytes = n_tot * (8 + R + 4 + 20 + R)
+    ms = sum(step_ms) / len(step_ms)
+    value = step_bytes / (ms * 1e-3) / 1e9
+    q = np.percentile(step_ms, [10, 50, 90])
+    n0 = wl.layer_numel[0]
+    result = {
+        "metric": "sync-group worker: one rank's outer-step kernels per round, GB/s of its own HBM bytes",
+        "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64", "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: {wl.description}", "units": wl.num_units, "unit_numel": n0,
+            "group_size": K, "rank": rank, "replica_dtype": wl.replica_dtype, "master_dtype": "f32",
+            "entry_point": "edit_group_norm + edit_group_weights + edit_group_apply per unit",
+            "collectives": "not this GPU's work; stood in for on the device: the all-gather by a copy of "
+                           "the rank's own pair into all K slots, the all-reduce by nothing (the rank's "
+                           "own fp32 export serves as Delta_bar)",
+            "bytes_per_element": 32 + 2 * R,
+            "parallelism": "one worker of a sync group with one replica per GPU",
+        },
+        "ms_p10": round(float(q[0]), 4), "ms_p50": round(float(q[1]), 4), "ms_p90": round(float(q[2]), 4),
+        "pct_peak_hbm": round(100 * value / PEAK_HBM_GBPS, 2),
+        "rollbacks_total": sum(int(st.rolled_back) for st in states),
+    }
+    if apply_ms:
+        per_launch = n0 * (4 + 20 + R)
+        avg = sum(apply_ms) / len(apply_ms)
+        achieved = per_launch / (avg * 1e-3) / 1e9
+        result["roofline"] = {
+            "kernel": "edit_group_apply (group_dbar + group_clip + group_update)", "bound": "hbm",
+            "achieved": round(achieved, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
+            "bytes_per_launch": per_launch, "avg_launch_ms": round(avg, 5), "sampled_launches": len(apply_ms),
+        }
+        norm_avg = sum(norm_ms) / len(norm_ms)
+        result["kernels_ms_avg"] = {
+            "norm_call": round(norm_avg, 5), "apply_call": round(avg, 5),
+            "norm_call_gbps": round(n0 * (8 + R) / (norm_avg * 1e-3) / 1e9, 2),
+        }
+    else:
+        result["roofline"] = None
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+def summarize_group_trace(out_dir: str, bench_json: str) -> str:
+    """profiles/ table of a rocprofv3 --kernel-trace --stats run of
+    `bench.py --sync-group-rank 0` (`<out>/prof_group/group_kernel_stats.csv`)."""
+    import csv
+
+    with open(bench_json) as f:
+        bench = json.load(f)
+    n, R = bench["config"]["unit_numel"], 2 if bench["config"]["replica_dtype"] == "bf16" else 4
+    algo = {"group_norm_kernel": n * (8 + R), "group_dbar_kernel": n * 4, "group_update_kernel": n * (20 + R)}
+    rows = []
+    with open(os.path.join(out_dir, "prof_group", "group_kernel_stats.csv")) as f:
+        for row in csv.DictReader(f):
+            name = row["Name"]
+            kind = next((k for k in ("group_norm_kernel", "group_self_kernel", "group_weights_kernel",
+                                     "group_clear_kernel", "group_dbar_kernel", "group_clip_kernel",
+                                     "group_update_kernel") if k in name), None)
+            if kind:
+                rows.append((kind, int(float(row["Calls"])), float(row["AverageNs"]) / 1e3,
+                             float(row["MinNs"]) / 1e3, float(row["MaxNs"]) / 1e3))
+    order = ["group_norm_kernel", "group_self_kernel", "group_weights_kernel", "group_clear_kernel",
+             "group_dbar_kernel", "group_clip_kernel", "group_update_kernel"]
+    rows.sort(key=lambda r: order.index(r[0]))
+    lines = [f"# Kernel durations: one sync-group worker (rank 0 of {bench['config']['group_size']}), "
+             f"{bench['config']['units']} units x {n:,} elements, {bench['config']['replica_dtype']} replica", "",
+             "Command (from the repository root; `<out>` = the directory the profiler wrote to):", "",
+             "    rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_group -o group -- "
+             "python bench.py --sync-group-rank 0", "",
+             "The collectives between the calls are stood in for on the device (see the bench's config).", "",
+             "| kernel | calls | avg us | min us | max us | algorithmic bytes | GB/s at avg |",
+             "|---|---|---|---|---|---|---|"]
+    for kind, calls, avg, mn, mx in rows:
+        b = algo.get(kind)
+        gbps = f"{b / (avg * 1e-6) / 1e9:.1f}" if b else "-"
+        lines.append(f"| {kind} | {calls} | {avg:.1f} | {mn:.1f} | {mx:.1f} | {b if b else '-'} | {gbps} |")
+    lines += ["", f"The traced run's own line: {bench['ms_per_step']} ms per step, {bench['value']} GB/s "
+              f"({bench['pct_peak_hbm']}% of 8 TB/s) on the rank's bytes."]
+    text = "\n".join(lines) + "\n"
+    with open(os.path.join(ROOT, "profiles", "sync_group_worker_1b_kernel_trace_stats.md"), "w") as f:
+        f.write(text)
+    return text
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[1])
     ap.add_argument("--gpus", type=int, default=1)
@@ -416,6 +576,9 @@ def main(argv=None) -> int:
     ap.add_argument("--shards", type=int, default=1,
                     help="split every unit into S shards that share one decision through "
                          "edit_outer_gram_layer / edit_outer_apply_layer (the module-norm path)")
+    ap.add_argument("--sync-group-rank", type=int, default=None, metavar="R",
+                    help="time rank R's share of a sync group whose K replicas sit on K GPUs "
+                         "(edit_group_*; the collectives stood in for on the device)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--profile-every", type=int, default=12,
                     help="record per-kernel HIP events on every k-th unit (0: none, roofline then null)")
@@ -431,6 +594,8 @@ def main(argv=None) -> int:
                     help="write profiles/ summaries from rocprofv3 CSVs under OUT_DIR (no GPU)")
     ap.add_argument("--profile-variant", default="two-pass", choices=("two-pass", "one-pass"),
                     help="which step --summarize-profiles reads (default: the two-pass step)")
+    ap.add_argument("--summarize-group-trace", nargs=2, metavar=("OUT_DIR", "BENCH_JSON"),
+                    help="write the profiles/ table of a traced --sync-group-rank run (no GPU)")
     ap.add_argument("--summarize-trace", nargs=2, metavar=("OUT_DIR", "WORKLOAD"),
                     help="write a per-unit-size kernel table from a rocprofv3 kernel trace (no GPU)")
     args = ap.parse_args(argv)
@@ -439,6 +604,9 @@ def main(argv=None) -> int:
         return 0
     if args.summarize_trace:
         print(summarize_trace_by_grid(*args.summarize_trace))
+        return 0
+    if args.summarize_group_trace:
+        print(summarize_group_trace(*args.summarize_group_trace))
         return 0
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -460,6 +628,8 @@ def main(argv=None) -> int:
     wl = synth.get(args.config)
     if args.units:
         wl = wl.with_units(range(args.units))
+    if args.sync_group_rank is not None:
+        return run_sync_group(args, torch, np, wl, dev)
     K, R = wl.num_workers, wl.replica_bytes
     hyper = wl.hyper()
     warm_rounds = hyper.pop("warmup_rounds")

@@ -218,6 +218,64 @@ const char *edit_outer_strerror(edit_status_t s);
 /* Message of the last failure on the calling thread ("" if none). */
 const char *edit_outer_last_error(void);
 
+/* ---- one worker of a sync group on its own GPU ------------------------- */
+
+/* In EDiT a module's K replicas belong to the K workers of a model sync
+ * group, one per GPU, and every worker runs Sync() (appendix, Algorithm 2)
+ * on its own copy: its pseudo gradient Delta_i and norm G_i, its z-test
+ * against its own EMA state (Eq. 1), an exchange of the K norms (the
+ * "sync the pseudo gradient norms" step), the weights (Eq. 2), the sum
+ * Delta_bar = sum_j w_j Delta_j over the group (Eq. 3), the clip (Eq. 4-5)
+ * and OuterOpt.  A group handle is one worker's (rank's) share of that on
+ * its GPU; the two exchanges between the calls are the caller's collectives
+ * (for instance RCCL over xGMI), which this library does not make:
+ *
+ *   edit_group_norm      Delta_rank = replica - theta in fp64: G_rank, this
+ *                        worker's z-test and EMA update, Delta_rank exported
+ *                        to `delta` in fp32, and {G_rank, flag} to `norm_out`
+ *   [caller] all-gather of every rank's norm_out, in rank order
+ *   edit_group_weights   the group's decision from the gathered pairs (mask,
+ *                        rollback, w_j; the same on every rank), w_rank to
+ *                        `weight_out`, and `delta` cleared when this worker
+ *                        is flagged (its Delta may be NaN; w_rank is then 0)
+ *   [caller] all-reduce sum over the group of w_j * delta_j (e.g. a
+ *            pre-multiplied sum with w_rank as this rank's factor) into dbar
+ *   edit_group_apply     Gbar = ||dbar||, beta, Nesterov on theta and the
+ *                        momentum, and this rank's replica set to theta'; on
+ *                        a rollback the replica is set to theta only
+ *
+ * Each call is enqueued on `stream` and reads what the previous call wrote
+ * through the caller's collectives on the same stream order.  The pseudo
+ * gradient's norm is exact (fp64); the collective's payload is fp32, so
+ * Delta_bar carries one fp32 rounding per term (relative 2^-24) against the
+ * single-GPU step.
+ *
+ * cfg is validated as by edit_outer_init (num_workers = K, the group size;
+ * EDIT_ONE_PASS is not accepted); 0 <= rank < K.  All tensor pointers are
+ * device pointers on the handle's device, 16-byte aligned (the 2-double
+ * norm_out / 2K-double gathered / 1-double weight_out: 8-byte aligned), with
+ * n = layer_numel[layer] elements: theta, momentum, delta and dbar fp32,
+ * replica of cfg->replica_dtype.  theta, momentum, replica and delta must not
+ * overlap each other; dbar may be `delta` itself (an in-place all-reduce)
+ * but must not overlap theta, momentum or the replica.  The EMA state of a
+ * group handle is this worker's only: edit_group_state_get reports it at
+ * index `rank` of ema_mean / ema_std (0 elsewhere), and the norms, mask and
+ * weights of every worker from the last decision. */
+typedef struct edit_group *edit_group_t; /* opaque, library-owned */
+
+edit_status_t edit_group_init(const edit_outer_config_t *cfg, int32_t rank, edit_group_t *out);
+edit_status_t edit_group_norm(edit_group_t h, int32_t layer, const float *theta, const void *replica,
+                              float *delta, double *norm_out, void *stream);
+edit_status_t edit_group_weights(edit_group_t h, int32_t layer, const double *gathered,
+                                 double *weight_out, float *delta, void *stream);
+edit_status_t edit_group_apply(edit_group_t h, int32_t layer, const float *dbar, float *theta,
+                               float *momentum, void *replica, void *stream);
+/* As edit_outer_state_get / _set, for this worker (see above); state_set
+ * takes ema_mean[rank], ema_std[rank] and round. */
+edit_status_t edit_group_state_get(edit_group_t h, int32_t layer, edit_layer_state_t *out);
+edit_status_t edit_group_state_set(edit_group_t h, int32_t layer, const edit_layer_state_t *in);
+void edit_group_destroy(edit_group_t h);
+
 /* ---- measurement helpers (not part of the method) ---------------------- */
 
 /* every > 0: steps of units whose index is a multiple of `every` record HIP

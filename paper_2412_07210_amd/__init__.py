@@ -5,6 +5,6 @@ of the work; `outer` is its Python binding and `synth` makes seeded
 synthetic workloads shaped like Llama decoder layers.
 """
 from .outer import (  # noqa: F401
-    AE, GC, ONE_PASS, WA, EditOuter, EditOuterError, LayerState, OuterConfig, copy_probe,
-    load_library,
+    AE, GC, ONE_PASS, WA, EditOuter, EditOuterError, LayerState, OuterConfig, SyncGroupWorker,
+    copy_probe, load_library,
 )

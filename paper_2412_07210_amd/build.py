@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIBRARY = os.path.join(PKG, "libedit_outer.so")
-SOURCES = ["edit_outer_kernels.hip", "edit_outer_runtime.hip"]
+SOURCES = ["edit_outer_kernels.hip", "edit_outer_runtime.hip", "edit_group_kernels.hip", "edit_group_runtime.hip"]
 ARCH = "gfx950"
 
 # -packed-fp32-ops off: no v_pk_* fp32 instructions are generated.

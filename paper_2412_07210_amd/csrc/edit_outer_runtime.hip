@@ -18,6 +18,13 @@
 #include <vector>
 
 #include "edit_outer_internal.h"
+#include "edit_group_internal.h"
+
+#define EDIT_TRY(expr)                    \
+  do {                                    \
+    const edit_status_t st_ = (expr);     \
+    if (st_ != EDIT_OK) return st_;       \
+  } while (0)
 
 using namespace edit;
 
@@ -131,26 +138,11 @@ void destroy_units(edit_outer* h) {
 
 }  // namespace
 
-extern "C" {
+namespace edit {
 
-const char* edit_outer_strerror(edit_status_t s) {
-  switch (s) {
-    case EDIT_OK: return "ok";
-    case EDIT_EINVAL: return "invalid argument";
-    case EDIT_ENOMEM: return "out of memory";
-    case EDIT_EHIP: return "HIP runtime error";
-    case EDIT_ESTATE: return "invalid state";
-    case EDIT_ENODEV: return "no gfx950 device";
-  }
-  return "unknown status";
-}
+edit_status_t set_error(edit_status_t s, const char* msg) { return fail(s, msg); }
 
-const char* edit_outer_last_error(void) { return g_last_error.c_str(); }
-
-edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out) {
-  g_last_error.clear();
-  if (!cfg || !out) return fail(EDIT_EINVAL, "cfg and out must not be NULL");
-  *out = nullptr;
+edit_status_t validate_config(const edit_outer_config_t* cfg) {
   const int K = cfg->num_workers;
   if (K < 1 || K > EDIT_MAX_K)
     return fail(EDIT_EINVAL, "num_workers must be in 1.." + std::to_string(EDIT_MAX_K));
@@ -173,7 +165,10 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
   for (int l = 0; l < cfg->num_layers; ++l)
     if (cfg->layer_numel[l] < 0)
       return fail(EDIT_EINVAL, "layer_numel[" + std::to_string(l) + "] is negative");
+  return EDIT_OK;
+}
 
+edit_status_t current_gfx950(int* device, int* num_cu) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
@@ -183,6 +178,38 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
   if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
     return fail(EDIT_ENODEV, std::string("device arch is ") + prop.gcnArchName +
                                  "; this library is built for gfx950 only");
+  *device = dev;
+  *num_cu = prop.multiProcessorCount;
+  return EDIT_OK;
+}
+
+}  // namespace edit
+
+extern "C" {
+
+const char* edit_outer_strerror(edit_status_t s) {
+  switch (s) {
+    case EDIT_OK: return "ok";
+    case EDIT_EINVAL: return "invalid argument";
+    case EDIT_ENOMEM: return "out of memory";
+    case EDIT_EHIP: return "HIP runtime error";
+    case EDIT_ESTATE: return "invalid state";
+    case EDIT_ENODEV: return "no gfx950 device";
+  }
+  return "unknown status";
+}
+
+const char* edit_outer_last_error(void) { return g_last_error.c_str(); }
+
+edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out) {
+  g_last_error.clear();
+  if (!cfg || !out) return fail(EDIT_EINVAL, "cfg and out must not be NULL");
+  *out = nullptr;
+  const int K = cfg->num_workers;
+  EDIT_TRY(validate_config(cfg));
+  int dev = 0, num_cu = 0;
+  EDIT_TRY(current_gfx950(&dev, &num_cu));
+  hipError_t e = hipSuccess;
 
   edit_outer* h = new (std::nothrow) edit_outer;
   if (!h) return fail(EDIT_ENOMEM, "host allocation failed");
@@ -190,7 +217,7 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
   h->numel.assign(cfg->layer_numel, cfg->layer_numel + cfg->num_layers);
   h->cfg.layer_numel = h->numel.data();
   h->device = dev;
-  h->num_cu = prop.multiProcessorCount;
+  h->num_cu = num_cu;
   const bool bf16 = cfg->replica_dtype == EDIT_BF16;
   h->cap1 = h->num_cu * pass1_blocks_per_cu(K, bf16);
   h->one_pass = (cfg->flags & EDIT_ONE_PASS) != 0;
@@ -407,11 +434,6 @@ struct Enqueue {
   }
 };
 
-#define EDIT_TRY(expr)                    \
-  do {                                    \
-    const edit_status_t st_ = (expr);     \
-    if (st_ != EDIT_OK) return st_;       \
-  } while (0)
 
 }  // namespace
 

@@ -33,6 +33,8 @@ EXPORTS = (
     "edit_outer_state_get", "edit_outer_state_set",
     "edit_outer_destroy", "edit_outer_strerror", "edit_outer_last_error",
     "edit_outer_set_profiling", "edit_outer_kernel_times", "edit_outer_copy_probe",
+    "edit_group_init", "edit_group_norm", "edit_group_weights", "edit_group_apply",
+    "edit_group_state_get", "edit_group_state_set", "edit_group_destroy",
 )
 
 
@@ -122,6 +124,20 @@ def load_library() -> ctypes.CDLL:
     lib.edit_outer_kernel_times.restype = st
     lib.edit_outer_copy_probe.argtypes = [vp, vp, ctypes.c_int64, vp]
     lib.edit_outer_copy_probe.restype = st
+    lib.edit_group_init.argtypes = [ctypes.POINTER(_Config), ctypes.c_int32, ctypes.POINTER(vp)]
+    lib.edit_group_init.restype = st
+    lib.edit_group_norm.argtypes = [vp, ctypes.c_int32, vp, vp, vp, vp, vp]
+    lib.edit_group_norm.restype = st
+    lib.edit_group_weights.argtypes = [vp, ctypes.c_int32, vp, vp, vp, vp]
+    lib.edit_group_weights.restype = st
+    lib.edit_group_apply.argtypes = [vp, ctypes.c_int32, vp, vp, vp, vp, vp]
+    lib.edit_group_apply.restype = st
+    lib.edit_group_state_get.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(_LayerState)]
+    lib.edit_group_state_get.restype = st
+    lib.edit_group_state_set.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(_LayerState)]
+    lib.edit_group_state_set.restype = st
+    lib.edit_group_destroy.argtypes = [vp]
+    lib.edit_group_destroy.restype = None
     _lib = lib
     return lib
 
@@ -159,6 +175,27 @@ class OuterConfig:
         return torch.bfloat16 if self.replica_dtype == "bf16" else torch.float32
 
 
+def _c_config(cfg: OuterConfig, numel: List[int]):
+    """The C configuration (and the element-count array it points to, which
+    must stay alive until the init call returns)."""
+    arr = (ctypes.c_int64 * len(numel))(*numel)
+    c = _Config(int(cfg.num_workers), len(numel), arr,
+                BF16 if cfg.replica_dtype == "bf16" else F32, int(cfg.flags),
+                float(cfg.outer_lr), float(cfg.momentum), float(cfg.clip_threshold),
+                float(cfg.clip_eps), float(cfg.ema_alpha), float(cfg.z_threshold),
+                int(cfg.ema_warmup_rounds))
+    return c, arr
+
+
+def _layer_state(st: "_LayerState", K: int) -> "LayerState":
+    return LayerState(
+        round=int(st.round), rolled_back=bool(st.rolled_back), z_tested=bool(st.z_tested),
+        ema_mean=np.array(st.ema_mean[:K]), ema_std=np.array(st.ema_std[:K]),
+        norm=np.array(st.norm[:K]), weight=np.array(st.weight[:K]),
+        anomalous=np.array(st.anomalous[:K], dtype=np.uint8),
+        synced_norm=float(st.synced_norm), clip_coef=float(st.clip_coef))
+
+
 @dataclass
 class LayerState:
     round: int
@@ -188,12 +225,7 @@ class EditOuter:
             raise ValueError("replica_dtype must be 'bf16' or 'f32'")
         lib = load_library()
         self._numel = [int(n) for n in cfg.layer_numel]
-        arr = (ctypes.c_int64 * len(self._numel))(*self._numel)
-        c = _Config(int(cfg.num_workers), len(self._numel), arr,
-                    BF16 if cfg.replica_dtype == "bf16" else F32, int(cfg.flags),
-                    float(cfg.outer_lr), float(cfg.momentum), float(cfg.clip_threshold),
-                    float(cfg.clip_eps), float(cfg.ema_alpha), float(cfg.z_threshold),
-                    int(cfg.ema_warmup_rounds))
+        c, arr = _c_config(cfg, self._numel)
         h = ctypes.c_void_p()
         with torch.cuda.device(self.device):
             _check(lib.edit_outer_init(ctypes.byref(c), ctypes.byref(h)), "edit_outer_init")
@@ -353,13 +385,7 @@ class EditOuter:
         with torch.cuda.device(self.device):
             _check(self._lib.edit_outer_state_get(self._h, int(layer), ctypes.byref(st)),
                    "edit_outer_state_get")
-        K = self.cfg.num_workers
-        return LayerState(
-            round=int(st.round), rolled_back=bool(st.rolled_back), z_tested=bool(st.z_tested),
-            ema_mean=np.array(st.ema_mean[:K]), ema_std=np.array(st.ema_std[:K]),
-            norm=np.array(st.norm[:K]), weight=np.array(st.weight[:K]),
-            anomalous=np.array(st.anomalous[:K], dtype=np.uint8),
-            synced_norm=float(st.synced_norm), clip_coef=float(st.clip_coef))
+        return _layer_state(st, self.cfg.num_workers)
 
     def state_set(self, layer: int, ema_mean: Sequence[float], ema_std: Sequence[float],
                   round_: int) -> None:
@@ -434,6 +460,116 @@ class RoundPlan:
         name = "edit_outer_step_round_host" if self._host else "edit_outer_step_round"
         fn = getattr(h._lib, name)
         _check(h._call(fn, self._count, self._layers, self._theta, self._mom, self._reps, s), name)
+
+
+class SyncGroupWorker:
+    """One worker (rank) of a sync group whose K replicas sit on K GPUs: its
+    share of the Sync() procedure on its own GPU (edit_group_* of the C ABI).
+    The all-gather of the norm pairs and the all-reduce of w_j * Delta_j
+    between the three calls are the caller's collectives."""
+
+    def __init__(self, cfg: OuterConfig, rank: int, device: Optional[torch.device] = None):
+        self.cfg = cfg
+        self.rank = int(rank)
+        device = torch.device("cuda") if device is None else torch.device(device)
+        if device.type != "cuda":
+            raise ValueError("the handle needs a GPU device")
+        if device.index is None:
+            device = torch.device("cuda", torch.cuda.current_device())
+        self.device = device
+        if cfg.replica_dtype not in ("bf16", "f32"):
+            raise ValueError("replica_dtype must be 'bf16' or 'f32'")
+        lib = load_library()
+        self._numel = [int(n) for n in cfg.layer_numel]
+        c, arr = _c_config(cfg, self._numel)
+        h = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            _check(lib.edit_group_init(ctypes.byref(c), self.rank, ctypes.byref(h)), "edit_group_init")
+        self._h = h
+        self._lib = lib
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            with torch.cuda.device(self.device):
+                self._lib.edit_group_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _arg(self, t: torch.Tensor, n: int, dtype: torch.dtype, what: str) -> int:
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{what} must be a torch.Tensor")
+        if t.device != self.device or t.dtype != dtype or not t.is_contiguous() or t.numel() != n:
+            raise ValueError(f"{what} must be a contiguous {dtype} tensor of {n} elements on {self.device}")
+        return t.data_ptr()
+
+    def _n(self, layer: int) -> int:
+        if not 0 <= layer < len(self._numel):
+            raise IndexError(f"layer {layer} out of range")
+        return self._numel[layer]
+
+    def _call(self, fn, what: str, *args) -> None:
+        with torch.cuda.device(self.device):
+            _check(fn(self._h, *args), what)
+
+    def norm(self, layer: int, theta: torch.Tensor, replica: torch.Tensor, delta: torch.Tensor,
+             norm_out: Optional[torch.Tensor] = None,
+             stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        """Enqueue the norm pass; returns norm_out = [G_rank, flag] (fp64,
+        device), this rank's part of the all-gather.  delta receives Delta_rank (fp32)."""
+        n = self._n(layer)
+        if norm_out is None:
+            norm_out = torch.empty(2, dtype=torch.float64, device=self.device)
+        self._call(self._lib.edit_group_norm, "edit_group_norm", int(layer),
+                   self._arg(theta, n, torch.float32, "theta"),
+                   self._arg(replica, n, self.cfg.torch_dtype, "replica"),
+                   self._arg(delta, n, torch.float32, "delta"),
+                   self._arg(norm_out, 2, torch.float64, "norm_out"), _stream_handle(stream, self.device))
+        return norm_out
+
+    def weights(self, layer: int, gathered: torch.Tensor, delta: torch.Tensor,
+                weight_out: Optional[torch.Tensor] = None,
+                stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        """Enqueue the group decision from the gathered [K, 2] pairs; returns
+        weight_out = [w_rank] (fp64, device).  delta is cleared if this rank is flagged."""
+        n = self._n(layer)
+        K = self.cfg.num_workers
+        if weight_out is None:
+            weight_out = torch.empty(1, dtype=torch.float64, device=self.device)
+        self._call(self._lib.edit_group_weights, "edit_group_weights", int(layer),
+                   self._arg(gathered, 2 * K, torch.float64, "gathered"),
+                   self._arg(weight_out, 1, torch.float64, "weight_out"),
+                   self._arg(delta, n, torch.float32, "delta"), _stream_handle(stream, self.device))
+        return weight_out
+
+    def apply(self, layer: int, dbar: torch.Tensor, theta: torch.Tensor, momentum: torch.Tensor,
+              replica: torch.Tensor, stream: Optional[torch.cuda.Stream] = None) -> None:
+        """Enqueue the clip and the update from the all-reduced dbar (in place
+        on theta, momentum and the replica)."""
+        n = self._n(layer)
+        self._call(self._lib.edit_group_apply, "edit_group_apply", int(layer),
+                   self._arg(dbar, n, torch.float32, "dbar"),
+                   self._arg(theta, n, torch.float32, "theta"),
+                   self._arg(momentum, n, torch.float32, "momentum"),
+                   self._arg(replica, n, self.cfg.torch_dtype, "replica"), _stream_handle(stream, self.device))
+
+    def state_get(self, layer: int) -> LayerState:
+        st = _LayerState()
+        self._call(self._lib.edit_group_state_get, "edit_group_state_get", int(layer), ctypes.byref(st))
+        return _layer_state(st, self.cfg.num_workers)
+
+    def state_set(self, layer: int, ema_mean: float, ema_std: float, round_: int) -> None:
+        """This worker's EMA pair and the round counter of unit `layer`."""
+        st = _LayerState()
+        st.round = int(round_)
+        st.num_workers = self.cfg.num_workers
+        st.ema_mean[self.rank] = float(ema_mean)
+        st.ema_std[self.rank] = float(ema_std)
+        self._call(self._lib.edit_group_state_set, "edit_group_state_set", int(layer), ctypes.byref(st))
 
 
 def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream: Optional[torch.cuda.Stream] = None) -> None:

@@ -15,7 +15,7 @@ HEADER = os.path.join(ROOT, "include", "edit_outer.h")
 def _declared():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(edit_outer_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(edit_(?:outer|group)_\w+)\s*\(", text)))
 
 
 def test_header_declarations_match_binding():
@@ -53,6 +53,7 @@ def test_strerror():
 
 def _init(**over):
     lib = outer.load_library()
+    rank = over.pop("rank", None)
     numel = over.pop("numel", [1024])
     arr = (ctypes.c_int64 * len(numel))(*numel)
     fields = dict(num_workers=4, num_layers=len(numel), layer_numel=arr, replica_dtype=1,
@@ -61,7 +62,10 @@ def _init(**over):
     fields.update(over)
     cfg = outer._Config(**fields)
     h = ctypes.c_void_p()
-    rc = lib.edit_outer_init(ctypes.byref(cfg), ctypes.byref(h))
+    if rank is None:
+        rc = lib.edit_outer_init(ctypes.byref(cfg), ctypes.byref(h))
+    else:
+        rc = lib.edit_group_init(ctypes.byref(cfg), rank, ctypes.byref(h))
     return rc, lib.edit_outer_last_error().decode()
 
 
@@ -87,6 +91,21 @@ def test_init_rejects_bad_config(over, needle):
     assert needle in msg
 
 
+@pytest.mark.parametrize("over,needle", [
+    (dict(rank=-1), "rank"),
+    (dict(rank=4), "rank"),
+    (dict(rank=0, flags=8), "EDIT_ONE_PASS"),
+    (dict(rank=0, num_workers=17), "num_workers"),
+    (dict(rank=0, ema_alpha=0.0), "ema_alpha"),
+    (dict(rank=1, numel=[5, -2]), "negative"),
+])
+def test_group_init_rejects_bad_config(over, needle):
+    """The sync-group worker validates like edit_outer_init, plus its rank."""
+    rc, msg = _init(**over)
+    assert rc == outer.EDIT_EINVAL
+    assert needle in msg
+
+
 def test_null_arguments_are_rejected():
     lib = outer.load_library()
     h = ctypes.c_void_p()
@@ -99,6 +118,13 @@ def test_null_arguments_are_rejected():
     assert lib.edit_outer_state_get(None, 0, None) == outer.EDIT_EINVAL
     assert lib.edit_outer_copy_probe(None, None, 15, None) == outer.EDIT_EINVAL
     lib.edit_outer_destroy(None)
+    assert lib.edit_group_init(None, 0, ctypes.byref(h)) == outer.EDIT_EINVAL
+    assert lib.edit_group_norm(None, 0, None, None, None, None, None) == outer.EDIT_EINVAL
+    assert lib.edit_group_weights(None, 0, None, None, None, None) == outer.EDIT_EINVAL
+    assert lib.edit_group_apply(None, 0, None, None, None, None, None) == outer.EDIT_EINVAL
+    assert lib.edit_group_state_get(None, 0, None) == outer.EDIT_EINVAL
+    assert lib.edit_group_state_set(None, 0, None) == outer.EDIT_EINVAL
+    lib.edit_group_destroy(None)
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
