@@ -1,8 +1,9 @@
 // The C ABI used directly from C++, without Python or PyTorch: device
 // buffers from hipMalloc, one outer round over two units through
 // edit_outer_step_round, the decision read back with edit_outer_state_get,
-// and the argument checks of the boundary.  Run by tests/test_gpu_c_abi.py;
-// built by __graft_entry__.build().
+// and the argument checks of the boundary; then the same round as K
+// sync-group workers (edit_group_*), the collectives done by hand.  Run by
+// tests/test_gpu_c_abi.py; built by __graft_entry__.build().
 //
 // The inputs make the expected result a closed form.  theta is a multiple of
 // 1/64 and worker j's replica is theta + (j + 1)/256 exactly (both exact in
@@ -145,6 +146,95 @@ int main() {
     (void)hipFree(mom[u]);
   }
   for (int k = 0; k < 2 * K; ++k) (void)hipFree(reps[k]);
+
+  // The same round as K sync-group workers (one replica each), the two
+  // collectives done by hand: the all-gather by copying the K pairs into
+  // one array, the all-reduce by forming sum_j w_j delta_j on the host.
+  {
+    const int64_t n = numel[0];
+    edit_outer_config_t gcfg = cfg;
+    gcfg.num_layers = 1;
+    edit_group_t g[K];
+    float *gth[K], *gmo[K], *gdelta[K], *dbar;
+    void* grep[K];
+    double *pair[K], *gathered, *wout[K];
+    for (int r = 0; r < K; ++r) {
+      CHECK(edit_group_init(&gcfg, r, &g[r]) == EDIT_OK, "group init: %s", edit_outer_last_error());
+      CHECK(hipMalloc(&gth[r], 4 * n) == hipSuccess && hipMalloc(&gmo[r], 4 * n) == hipSuccess &&
+                hipMalloc(&gdelta[r], 4 * n) == hipSuccess && hipMalloc(&grep[r], 2 * n) == hipSuccess &&
+                hipMalloc(&pair[r], 16) == hipSuccess && hipMalloc(&wout[r], 8) == hipSuccess,
+            "hipMalloc");
+      CHECK(hipMemcpy(gth[r], theta_h[0].data(), 4 * n, hipMemcpyHostToDevice) == hipSuccess, "copy");
+      CHECK(hipMemset(gmo[r], 0, 4 * n) == hipSuccess, "memset");
+      std::vector<uint16_t> rr(n);
+      for (int64_t i = 0; i < n; ++i) rr[i] = to_bf16_exact(theta_h[0][i] + (r + 1) / 256.0f);
+      CHECK(hipMemcpy(grep[r], rr.data(), 2 * n, hipMemcpyHostToDevice) == hipSuccess, "copy");
+    }
+    CHECK(hipMalloc(&gathered, 16 * K) == hipSuccess && hipMalloc(&dbar, 4 * n) == hipSuccess, "hipMalloc");
+    for (int r = 0; r < K; ++r)
+      CHECK(edit_group_norm(g[r], 0, gth[r], grep[r], gdelta[r], pair[r], nullptr) == EDIT_OK, "norm: %s",
+            edit_outer_last_error());
+    for (int r = 0; r < K; ++r)  // the all-gather
+      CHECK(hipMemcpy(gathered + 2 * r, pair[r], 16, hipMemcpyDeviceToDevice) == hipSuccess, "gather");
+    for (int r = 0; r < K; ++r)
+      CHECK(edit_group_weights(g[r], 0, gathered, wout[r], gdelta[r], nullptr) == EDIT_OK, "weights: %s",
+            edit_outer_last_error());
+    // the all-reduce: dbar = sum_r w_r delta_r, on the host in fp32
+    std::vector<float> acc(n, 0.f), d(n);
+    double w[K], G[K], sum_e = 0.0, cbar = 0.0;
+    for (int r = 0; r < K; ++r) {
+      CHECK(hipMemcpy(&w[r], wout[r], 8, hipMemcpyDeviceToHost) == hipSuccess, "copy back");
+      CHECK(hipMemcpy(d.data(), gdelta[r], 4 * n, hipMemcpyDeviceToHost) == hipSuccess, "copy back");
+      for (int64_t i = 0; i < n; ++i) acc[i] += static_cast<float>(w[r]) * d[i];
+      G[r] = (r + 1) / 256.0 * std::sqrt(static_cast<double>(n));
+      sum_e += std::exp(-(G[r] - G[0]));
+    }
+    for (int r = 0; r < K; ++r) {
+      const double expect_w = std::exp(-(G[r] - G[0])) / sum_e;
+      CHECK(std::fabs(w[r] - expect_w) <= 1e-12, "group w_%d %.17g vs %.17g", r, w[r], expect_w);
+      cbar += expect_w * (r + 1) / 256.0;
+    }
+    CHECK(hipMemcpy(dbar, acc.data(), 4 * n, hipMemcpyHostToDevice) == hipSuccess, "copy");
+    for (int r = 0; r < K; ++r)
+      CHECK(edit_group_apply(g[r], 0, dbar, gth[r], gmo[r], grep[r], nullptr) == EDIT_OK, "apply: %s",
+            edit_outer_last_error());
+    CHECK(hipDeviceSynchronize() == hipSuccess, "sync");
+    for (int r = 0; r < K; ++r) {
+      edit_layer_state_t st;
+      CHECK(edit_group_state_get(g[r], 0, &st) == EDIT_OK, "group state_get: %s", edit_outer_last_error());
+      CHECK(st.round == 1 && !st.rolled_back && st.clip_coef == 1.0, "rank %d: round/rollback/beta", r);
+      CHECK(std::fabs(st.norm[r] - G[r]) <= 1e-12 * G[r], "rank %d: G", r);
+      CHECK(std::fabs(st.ema_mean[r] - 0.02 * G[r]) <= 1e-12 * G[r], "rank %d: mu", r);
+      const double gbar = cbar * std::sqrt(static_cast<double>(n));
+      CHECK(std::fabs(st.synced_norm - gbar) <= 1e-6 * gbar, "rank %d: Gbar %.9g vs %.9g", r, st.synced_norm, gbar);
+      std::vector<float> th(n), b(n);
+      CHECK(hipMemcpy(th.data(), gth[r], 4 * n, hipMemcpyDeviceToHost) == hipSuccess, "copy back");
+      CHECK(hipMemcpy(b.data(), gmo[r], 4 * n, hipMemcpyDeviceToHost) == hipSuccess, "copy back");
+      for (int64_t i = 0; i < n; ++i) {
+        const double expect = theta_h[0][i] + nu * (1.0 + rho) * cbar;
+        CHECK(std::fabs(th[i] - expect) <= 1e-6 * (std::fabs(expect) + 1e-3), "rank %d theta[%lld]", r,
+              (long long)i);
+        CHECK(std::fabs(b[i] + cbar) <= 1e-6 * cbar, "rank %d b[%lld]", r, (long long)i);
+      }
+    }
+    // argument checks of the group entry points
+    edit_group_t bad = nullptr;
+    CHECK(edit_group_init(&gcfg, K, &bad) == EDIT_EINVAL, "rank K accepted");
+    CHECK(edit_group_norm(g[0], 1, gth[0], grep[0], gdelta[0], pair[0], nullptr) == EDIT_EINVAL, "bad layer accepted");
+    CHECK(edit_group_norm(g[0], 0, gth[0], grep[0], gth[0], pair[0], nullptr) == EDIT_EINVAL, "aliasing accepted");
+    CHECK(edit_group_apply(g[0], 0, gth[0], gth[0], gmo[0], grep[0], nullptr) == EDIT_EINVAL, "dbar aliasing accepted");
+    for (int r = 0; r < K; ++r) {
+      edit_group_destroy(g[r]);
+      (void)hipFree(gth[r]);
+      (void)hipFree(gmo[r]);
+      (void)hipFree(gdelta[r]);
+      (void)hipFree(grep[r]);
+      (void)hipFree(pair[r]);
+      (void)hipFree(wout[r]);
+    }
+    (void)hipFree(gathered);
+    (void)hipFree(dbar);
+  }
   std::printf("ok\n");
   return 0;
 }
