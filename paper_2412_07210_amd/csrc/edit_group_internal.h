@@ -40,10 +40,11 @@ hipError_t launch_group_norm(bool bf16, int rows, const float* theta, const void
                              int64_t n, double* partials, hipStream_t stream);
 hipError_t launch_group_self(const double* partials, int rows, GroupRecord* rec, double* norm_out,
                              const GroupParams& prm, hipStream_t stream);
-hipError_t launch_group_weights(const double* gathered, int K, int rank, GroupRecord* rec,
-                                double* weight_out, const GroupParams& prm, hipStream_t stream);
-hipError_t launch_group_clear(int blocks, const GroupRecord* rec, float* delta, int64_t n,
-                              hipStream_t stream);
+// `blocks` blocks: block 0 takes the decision; all of them clear `delta`
+// when this worker is flagged.
+hipError_t launch_group_weights(int blocks, const double* gathered, int K, int rank, GroupRecord* rec,
+                                double* weight_out, float* delta, int64_t n, const GroupParams& prm,
+                                hipStream_t stream);
 hipError_t launch_group_dbar(int rows, const GroupRecord* rec, const float* dbar, int64_t n,
                              double* partials, hipStream_t stream);
 hipError_t launch_group_clip(const double* partials, int rows, GroupRecord* rec, const GroupParams& prm,

@@ -10,11 +10,11 @@
 //   group_self      one block: the fixed-order sum of those partials, G_rank,
 //                   the z-test and EMA update of this worker (Eq. 1), and the
 //                   pair {G_rank, flag} for the group's all-gather;
-//   group_weights   one wave: the decision of all K workers from the gathered
+//   group_weights   the first wave of block 0: the decision of all K workers from the gathered
 //                   pairs (mask, rollback, softmax weights of Eq. 2), the same
-//                   on every rank;
-//   group_clear     a flagged worker's export set to zero, so its (possibly
-//                   non-finite) pseudo gradient never enters the sum;
+//                   on every rank; in the same launch a flagged worker's
+//                   export is set to zero, so its (possibly non-finite)
+//                   pseudo gradient never enters the sum;
 //   group_dbar      streams the all-reduced Delta_bar: per-block partials of
 //                   its squared norm;
 //   group_clip      one block: Gbar and beta (Eq. 4);
@@ -247,14 +247,29 @@ __global__ __launch_bounds__(kGroupOneBlock) void group_self_kernel(const double
 
 // ---------------------------------------------------------- group_weights
 
-// The decision of the whole group from the gathered pairs, taken by one wave
-// (worker j in lane j) in the same order on every rank: mask, rollback,
-// weights (Eq. 2; the softmax of -G over the unflagged workers, shifted by
-// their smallest norm), and this worker's weight for the all-reduce.
-__global__ __launch_bounds__(64) void group_weights_kernel(const double* __restrict__ gathered, int K,
-                                                         int rank, GroupRecord* rec,
-                                                         double* __restrict__ weight_out,
-                                                         GroupParams prm) {
+// The decision of the whole group from the gathered pairs, taken by the first
+// wave of block 0 (worker j in lane j) in the same order on every rank: mask,
+// rollback, weights (Eq. 2; the softmax of -G over the unflagged workers,
+// shifted by their smallest norm), and this worker's weight for the
+// all-reduce.  In the same launch every block clears its share of this
+// worker's export when the worker was flagged by its own z-test (known from
+// the earlier group_self launch), so its possibly non-finite pseudo gradient
+// never enters the sum; otherwise those blocks return at once.
+__global__ __launch_bounds__(kGroupThreads) void group_weights_kernel(const double* __restrict__ gathered, int K,
+                                                                     int rank, GroupRecord* rec,
+                                                                     double* __restrict__ weight_out,
+                                                                     float* __restrict__ delta, int64_t n,
+                                                                     GroupParams prm) {
+  if (rec->self_flag) {  // grid-stride over 16-byte vectors, then the tail
+    const int64_t nvec = n / 4;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kGroupThreads;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    for (int64_t v = static_cast<int64_t>(blockIdx.x) * kGroupThreads + threadIdx.x; v < nvec; v += stride)
+      reinterpret_cast<f32x4*>(delta)[v] = z;
+    const int64_t i = nvec * 4 + threadIdx.x;
+    if (blockIdx.x == 0 && i < n) delta[i] = 0.f;
+  }
+  if (blockIdx.x != 0 || threadIdx.x >= 64) return;
   const int lane = threadIdx.x;
   const bool mine = lane < K;
   const double G = mine ? gathered[2 * lane] : 0.0;
@@ -287,20 +302,6 @@ __global__ __launch_bounds__(64) void group_weights_kernel(const double* __restr
     rec->clip_coef = 0.0;
     weight_out[0] = w_rank;
   }
-}
-
-// A flagged worker's export set to zero (every block returns at once
-// otherwise).  Grid-stride over 16-byte vectors, then the tail.
-__global__ __launch_bounds__(kGroupThreads) void group_clear_kernel(const GroupRecord* __restrict__ rec,
-                                                                   float* __restrict__ delta, int64_t n) {
-  if (!rec->self_flag) return;  // block-uniform
-  const int64_t nvec = n / 4;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kGroupThreads;
-  const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-  for (int64_t v = static_cast<int64_t>(blockIdx.x) * kGroupThreads + threadIdx.x; v < nvec; v += stride)
-    reinterpret_cast<f32x4*>(delta)[v] = z;
-  const int64_t i = nvec * 4 + threadIdx.x;
-  if (blockIdx.x == 0 && i < n) delta[i] = 0.f;
 }
 
 // ------------------------------------------------------------- group_dbar
@@ -423,15 +424,11 @@ hipError_t launch_group_self(const double* partials, int rows, GroupRecord* rec,
   return hipGetLastError();
 }
 
-hipError_t launch_group_weights(const double* gathered, int K, int rank, GroupRecord* rec, double* weight_out,
-                                const GroupParams& prm, hipStream_t stream) {
-  hipLaunchKernelGGL(group_weights_kernel, dim3(1), dim3(64), 0, stream, gathered, K, rank, rec, weight_out,
-                     prm);
-  return hipGetLastError();
-}
-
-hipError_t launch_group_clear(int blocks, const GroupRecord* rec, float* delta, int64_t n, hipStream_t stream) {
-  hipLaunchKernelGGL(group_clear_kernel, dim3(blocks), dim3(kGroupThreads), 0, stream, rec, delta, n);
+hipError_t launch_group_weights(int blocks, const double* gathered, int K, int rank, GroupRecord* rec,
+                                double* weight_out, float* delta, int64_t n, const GroupParams& prm,
+                                hipStream_t stream) {
+  hipLaunchKernelGGL(group_weights_kernel, dim3(blocks), dim3(kGroupThreads), 0, stream, gathered, K, rank, rec,
+                     weight_out, delta, n, prm);
   return hipGetLastError();
 }
 

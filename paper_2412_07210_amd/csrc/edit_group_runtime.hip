@@ -39,7 +39,7 @@ struct GUnit {
   int rows_norm = 1;   // blocks (= partials) of the norm pass
   int rows_dbar = 1;   // blocks (= partials) of the Delta_bar pass
   int blocks_up = 1;   // blocks of the update pass
-  int blocks_clear = 1;
+  int blocks_clear = 1;  // blocks of the decision launch (which clears a flagged export)
   double* part_norm = nullptr;
   double* part_dbar = nullptr;
   GroupRecord* rec = nullptr;
@@ -188,7 +188,7 @@ edit_status_t edit_group_init(const edit_outer_config_t* cfg, int32_t rank, edit
     u.rows_norm = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(cap_norm, gceil_div(nvec, kGroupThreads))));
     u.rows_dbar = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(cap_dbar, gceil_div(u.n / 4, kGroupThreads))));
     u.blocks_up = static_cast<int>(std::max<int64_t>(1, gceil_div(nvec, kGroupUpdateThreads)));
-    u.blocks_clear = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(num_cu * 4, gceil_div(u.n / 4, kGroupThreads))));
+    u.blocks_clear = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(num_cu, gceil_div(u.n / 4, kGroupThreads))));
     offs[l] = total;
     total += rec_bytes + ((sizeof(double) * (u.rows_norm + u.rows_dbar) + 255) & ~size_t(255));
   }
@@ -253,8 +253,8 @@ edit_status_t edit_group_weights(edit_group_t h, int32_t layer, const double* ga
   GROUP_TRY(check_disjoint(r, 3, "gathered, weight_out and delta must not overlap"));
   GROUP_TRY(check_group_device(h));
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = launch_group_weights(gathered, K, h->rank, u.rec, weight_out, group_params(h), s);
-  if (e == hipSuccess && n > 0) e = launch_group_clear(u.blocks_clear, u.rec, delta, n, s);
+  hipError_t e = launch_group_weights(u.blocks_clear, gathered, K, h->rank, u.rec, weight_out, delta, n,
+                                      group_params(h), s);
   if (e != hipSuccess) return gfail_hip(e, "group weights launch");
   u.has_state = true;
   return record_done(h, layer, s);
