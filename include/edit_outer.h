@@ -134,9 +134,9 @@ edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float *theta,
 /* One outer round: `count` distinct units, stepped in the given (forward)
  * order on `stream` (the layer-wise synchronization of Sec. 3.1), with the
  * same results bit for bit as calling edit_outer_step_layer for each of them
- * in that order.  A large unit is enqueued as pass 1, decision, pass 2 back
- * to back; a small unit's (pass 1 under 32 MB) one-block decision instead
- * runs inside the next unit's pass-1 launch, saving its own launch.
+ * in that order.  Each unit's one-block decision runs inside the next unit's
+ * pass-1 launch (an extra block), and its update pass follows that launch;
+ * only the last unit's decision runs as a kernel of its own.
  *   layers   [count] unit indices, each at most once (else EDIT_EINVAL)
  *   theta    [count] device pointers, as in edit_outer_step_layer
  *   momentum [count] device pointers

@@ -791,12 +791,12 @@ __device__ __forceinline__ void update_vector(float* theta, float* mom, const Mu
   for (int j = 0; j < K; ++j) st16<NT>(reinterpret_cast<u32x4*>(reps.p[j]) + v, out);
 }
 
-// One 16-byte vector of every buffer per thread, one block per 128 vectors,
-// blocks taken from the unit's end: the hardware dispatcher then keeps the
-// in-flight window of each of the 2K+4 streams short and ordered (measured
-// 5.5 TB/s here against 4.9 TB/s for a persistent grid-stride loop; 128-
-// thread blocks edged out 256), and the first blocks read what pass 1 read
-// last, still in the Infinity Cache.
+// One 16-byte vector of every buffer per thread, one block per 128 vectors
+// (a flat grid): the hardware dispatcher then keeps the in-flight window of
+// each of the 2K+4 streams short and ordered (measured 5.5 TB/s here against
+// 4.9 TB/s for a persistent grid-stride loop; 128-thread blocks edged out
+// 256).  Blocks are taken from the unit's end; forward order measured the
+// same.
 template <int K, bool BF16, bool NT>
 __global__ __launch_bounds__(kPass2Threads) void pass2_update_kernel(float* __restrict__ theta,
                                                                 float* __restrict__ mom,
