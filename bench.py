@@ -260,13 +260,18 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
     spans.sort()
     ours = {"pass1_gram_kernel", "pass1_gram_mfma_kernel", "decide_kernel", "pass2_update_kernel",
             "fused_mean_kernel", "fused_finish_kernel"}
-    gaps = sorted(b[0] - a[1] for a, b in zip(spans, spans[1:]) if a[2] in ours and b[2] in ours)
+    pairs = [(a[2], b[2], b[0] - a[1]) for a, b in zip(spans, spans[1:]) if a[2] in ours and b[2] in ours]
+    gaps = sorted(g for _, _, g in pairs)
     if gaps:
         med = gaps[len(gaps) // 2]
         lines += ["", f"Gap between consecutive dispatches of the method's kernels (end of one to start "
                   f"of the next, same stream): median {med / 1e3:.2f} us, 10th percentile "
                   f"{gaps[len(gaps) // 10] / 1e3:.2f} us, 90th {gaps[9 * len(gaps) // 10] / 1e3:.2f} us "
-                  f"over {len(gaps)} pairs."]
+                  f"over {len(gaps)} pairs.", "", "| from | to | pairs | median gap us | 90th us |",
+                  "|---|---|---|---|---|"]
+        for a, b in sorted({(a, b) for a, b, _ in pairs}):
+            g = sorted(x for pa, pb, x in pairs if (pa, pb) == (a, b))
+            lines.append(f"| {a} | {b} | {len(g)} | {g[len(g) // 2] / 1e3:.2f} | {g[9 * len(g) // 10] / 1e3:.2f} |")
     lines += ["", "The trace's VGPR_Count, Accum_VGPR_Count and LDS bytes per block (VGPR_Count reads "
               "half the compiler's per-lane VGPR figure on this ROCm, e.g. 60 for a 119-VGPR kernel):", ""]
     for kind, (v, a, l) in sorted(regs.items()):

@@ -271,7 +271,9 @@ edit_status_t edit_group_weights(edit_group_t h, int32_t layer, const double *ga
 edit_status_t edit_group_apply(edit_group_t h, int32_t layer, const float *dbar, float *theta,
                                float *momentum, void *replica, void *stream);
 /* As edit_outer_state_get / _set, for this worker (see above); state_set
- * takes ema_mean[rank], ema_std[rank] and round. */
+ * takes ema_mean[rank], ema_std[rank] and round.  Both wait for the unit's
+ * last edit_group_apply; after a norm or weights call that no apply has
+ * followed yet they synchronise the whole device instead. */
 edit_status_t edit_group_state_get(edit_group_t h, int32_t layer, edit_layer_state_t *out);
 edit_status_t edit_group_state_set(edit_group_t h, int32_t layer, const edit_layer_state_t *in);
 void edit_group_destroy(edit_group_t h);

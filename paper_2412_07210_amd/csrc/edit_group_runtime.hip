@@ -44,7 +44,8 @@ struct GUnit {
   double* part_dbar = nullptr;
   GroupRecord* rec = nullptr;
   hipEvent_t done = nullptr;
-  bool pending = false;
+  bool pending = false;     // `done` marks the unit's last edit_group_apply
+  bool unrecorded = false;  // a norm or weights call was enqueued after it
   bool has_state = false;
 };
 
@@ -130,18 +131,28 @@ GroupParams group_params(const edit_group* h) {
   return p;
 }
 
+// Only the last call of a step (edit_group_apply) records the unit's
+// completion event: an event record costs a few microseconds of stream time.
 edit_status_t record_done(edit_group* h, int32_t layer, hipStream_t s) {
   GUnit& u = h->units[layer];
   const hipError_t e = hipEventRecord(u.done, s);
   if (e != hipSuccess) return gfail_hip(e, "hipEventRecord");
   u.pending = true;
+  u.unrecorded = false;
   return EDIT_OK;
 }
 
+// Wait for the unit's enqueued work, then copy its record to the host.  After
+// a norm or weights call that no apply has followed yet there is no event to
+// wait on, so the whole device is synchronised instead.
 edit_status_t wait_and_read(edit_group* h, int32_t layer, GroupRecord* rec) {
   GUnit& u = h->units[layer];
   hipError_t e = hipSuccess;
-  if (u.pending && (e = hipEventSynchronize(u.done)) != hipSuccess) return gfail_hip(e, "hipEventSynchronize");
+  if (u.unrecorded) {
+    if ((e = hipDeviceSynchronize()) != hipSuccess) return gfail_hip(e, "hipDeviceSynchronize");
+  } else if (u.pending && (e = hipEventSynchronize(u.done)) != hipSuccess) {
+    return gfail_hip(e, "hipEventSynchronize");
+  }
   if ((e = hipMemcpy(rec, u.rec, sizeof *rec, hipMemcpyDeviceToHost)) != hipSuccess)
     return gfail_hip(e, "hipMemcpy D2H");
   return EDIT_OK;
@@ -236,7 +247,8 @@ edit_status_t edit_group_norm(edit_group_t h, int32_t layer, const float* theta,
   if (e == hipSuccess) e = launch_group_self(u.part_norm, u.rows_norm, u.rec, norm_out, group_params(h), s);
   if (e != hipSuccess) return gfail_hip(e, "group norm launch");
   u.has_state = true;
-  return record_done(h, layer, s);
+  u.unrecorded = true;
+  return EDIT_OK;
 }
 
 edit_status_t edit_group_weights(edit_group_t h, int32_t layer, const double* gathered, double* weight_out,
@@ -257,7 +269,8 @@ edit_status_t edit_group_weights(edit_group_t h, int32_t layer, const double* ga
                                       group_params(h), s);
   if (e != hipSuccess) return gfail_hip(e, "group weights launch");
   u.has_state = true;
-  return record_done(h, layer, s);
+  u.unrecorded = true;
+  return EDIT_OK;
 }
 
 edit_status_t edit_group_apply(edit_group_t h, int32_t layer, const float* dbar, float* theta, float* momentum,
@@ -335,8 +348,12 @@ void edit_group_destroy(edit_group_t h) {
   if (!h) return;
   int prev = -1;
   if (hipGetDevice(&prev) == hipSuccess && prev != h->device) (void)hipSetDevice(h->device);
-  for (GUnit& u : h->units)
+  bool unrecorded = false;
+  for (GUnit& u : h->units) {
+    unrecorded = unrecorded || u.unrecorded;
     if (u.pending) (void)hipEventSynchronize(u.done);
+  }
+  if (unrecorded) (void)hipDeviceSynchronize();
   destroy_group_units(h);
   if (prev >= 0 && prev != h->device) (void)hipSetDevice(prev);
   delete h;

@@ -49,7 +49,9 @@ struct Unit {
   UnitRecord* rec = nullptr;
   hipEvent_t done = nullptr;
   hipEvent_t prof[4] = {nullptr, nullptr, nullptr, nullptr};
-  bool pending = false;   // `done` has been recorded at least once
+  bool pending = false;   // a completion to wait for has been recorded
+  int done_slot = -1;     // -1: `done` (a single step); else the round-event slot
+  uint64_t done_gen = 0;  // generation of that slot's record the unit belongs to
   bool profiled = false;  // prof[] hold the last step's timestamps
   bool has_state = false; // stepped or state_set at least once
 };
@@ -89,6 +91,17 @@ struct edit_outer {
   bool one_pass = false;
   Offload off;
   std::vector<Unit> units;
+  // Completion of a round: one event recorded after its last kernel, shared
+  // by its units (an event record costs a few microseconds of stream time,
+  // one per unit would cost ~1% of a 1B round).  A ring of slots; before a
+  // slot is recorded again the host waits for its previous record, so every
+  // generation up to round_complete[slot] is known to have finished.
+  static constexpr int kRoundEvents = 4;
+  hipEvent_t round_ev[kRoundEvents] = {};
+  uint64_t round_gen[kRoundEvents] = {};       // generation of the slot's latest record
+  uint64_t round_complete[kRoundEvents] = {};  // generations <= this have finished
+  uint64_t next_gen = 1;
+  int next_slot = 0;
 };
 
 namespace {
@@ -126,6 +139,11 @@ void destroy_offload(edit_outer* h) {
 
 void destroy_units(edit_outer* h) {
   destroy_offload(h);
+  for (hipEvent_t& ev : h->round_ev)
+    if (ev) {
+      (void)hipEventDestroy(ev);
+      ev = nullptr;
+    }
   for (Unit& u : h->units) {
     if (u.done) (void)hipEventDestroy(u.done);
     for (hipEvent_t& ev : u.prof)
@@ -368,7 +386,8 @@ struct Enqueue {
   edit_status_t event(Unit& u, int32_t layer, int k) {
     if (!profiled(layer)) return EDIT_OK;
     hipError_t e = hipSuccess;
-    if (!u.prof[k] && (e = hipEventCreate(&u.prof[k])) != hipSuccess)
+    // timing only: no system-scope fence (it would add stream time)
+    if (!u.prof[k] && (e = hipEventCreateWithFlags(&u.prof[k], hipEventDisableSystemFence)) != hipSuccess)
       return fail_hip(e, "hipEventCreate");
     if ((e = hipEventRecord(u.prof[k], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
     return EDIT_OK;
@@ -424,11 +443,52 @@ struct Enqueue {
     hipError_t e = hipEventRecord(u.done, s);
     if (e != hipSuccess) return fail_hip(e, "hipEventRecord");
     u.pending = true;
+    u.done_slot = -1;
     u.profiled = profiled(layer);
     u.has_state = true;
     return EDIT_OK;
   }
+  // The end of a round: one event for all of its units.
+  edit_status_t finish_round(const int32_t* layers, int32_t count) {
+    const int slot = h->next_slot;
+    h->next_slot = (slot + 1) % edit_outer::kRoundEvents;
+    hipError_t e = hipSuccess;
+    if (!h->round_ev[slot] && (e = hipEventCreateWithFlags(&h->round_ev[slot], hipEventDisableTiming)) != hipSuccess)
+      return fail_hip(e, "hipEventCreate");
+    if (h->round_gen[slot] > h->round_complete[slot]) {  // its previous round may still run
+      if ((e = hipEventSynchronize(h->round_ev[slot])) != hipSuccess) return fail_hip(e, "hipEventSynchronize");
+      h->round_complete[slot] = h->round_gen[slot];
+    }
+    if ((e = hipEventRecord(h->round_ev[slot], s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+    const uint64_t gen = h->next_gen++;
+    h->round_gen[slot] = gen;
+    for (int32_t i = 0; i < count; ++i) {
+      Unit& u = h->units[layers[i]];
+      u.pending = true;
+      u.done_slot = slot;
+      u.done_gen = gen;
+      u.profiled = profiled(layers[i]);
+      u.has_state = true;
+    }
+    return EDIT_OK;
+  }
 };
+
+// Wait until the last enqueued step of `u` has finished.
+edit_status_t wait_unit(edit_outer* h, Unit& u) {
+  if (!u.pending) return EDIT_OK;
+  hipError_t e = hipSuccess;
+  if (u.done_slot < 0) {
+    e = hipEventSynchronize(u.done);
+  } else {
+    const int slot = u.done_slot;
+    if (h->round_complete[slot] >= u.done_gen) return EDIT_OK;
+    // not recorded again since (that would have completed this generation)
+    e = hipEventSynchronize(h->round_ev[slot]);
+    if (e == hipSuccess) h->round_complete[slot] = h->round_gen[slot];
+  }
+  return e == hipSuccess ? EDIT_OK : fail_hip(e, "hipEventSynchronize");
+}
 
 
 }  // namespace
@@ -527,8 +587,7 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
       EDIT_TRY(q.event(h->units[l], l, 3));
     }
     EDIT_TRY(q.records(0, h->cfg.num_layers));
-    for (int32_t i = 0; i < count; ++i) EDIT_TRY(q.finish(layers[i]));
-    return EDIT_OK;
+    return q.finish_round(layers, count);
   }
   // Every unit's decision rides in the next unit's pass-1 launch (one extra
   // block, which would otherwise idle), and its pass 2 follows that launch;
@@ -542,8 +601,7 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
     void* const* reps = replicas + static_cast<size_t>(i) * K;
     EDIT_TRY(q.event(h->units[l], l, 2));
     EDIT_TRY(q.pass2(l, theta[i], momentum[i], reps));
-    EDIT_TRY(q.event(h->units[l], l, 3));
-    return q.finish(l);
+    return q.event(h->units[l], l, 3);
   };
   for (int32_t i = 0; i < count; ++i) {
     const int32_t l = layers[i];
@@ -559,7 +617,7 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
     EDIT_TRY(q.decide(layers[pending]));
     EDIT_TRY(flush_pass2(pending));
   }
-  return EDIT_OK;
+  return q.finish_round(layers, count);
 }
 
 }  // extern "C"
@@ -680,7 +738,6 @@ edit_status_t edit_outer_step_round_host(edit_outer_t h, int32_t count, const in
       EDIT_TRY(q.pass2(l, dth, db, reps));
     }
     EDIT_TRY(q.event(u, l, 3));
-    EDIT_TRY(q.finish(l));
     // copy out once the step is done
     if ((e = hipEventRecord(o.comp_done[s], cs)) != hipSuccess ||
         (e = hipStreamWaitEvent(o.d2h, o.comp_done[s], 0)) != hipSuccess)
@@ -698,7 +755,7 @@ edit_status_t edit_outer_step_round_host(edit_outer_t h, int32_t count, const in
   for (int s = 0; s < kOffloadSlots; ++s)
     if (used_now[s] && (e = hipStreamWaitEvent(cs, o.out_done[s], 0)) != hipSuccess)
       return fail_hip(e, "round end");
-  return EDIT_OK;
+  return q.finish_round(layers, count);
 }
 
 edit_status_t edit_outer_state_get(edit_outer_t h, int32_t layer, edit_layer_state_t* out) {
@@ -709,9 +766,8 @@ edit_status_t edit_outer_state_get(edit_outer_t h, int32_t layer, edit_layer_sta
   if (!u.has_state) return fail(EDIT_ESTATE, "unit has neither stepped nor had its state set");
   edit_status_t st = check_device(h);
   if (st != EDIT_OK) return st;
+  EDIT_TRY(wait_unit(h, u));
   hipError_t e = hipSuccess;
-  if (u.pending && (e = hipEventSynchronize(u.done)) != hipSuccess)
-    return fail_hip(e, "hipEventSynchronize");
   UnitRecord rec;
   if ((e = hipMemcpy(&rec, u.rec, sizeof rec, hipMemcpyDeviceToHost)) != hipSuccess)
     return fail_hip(e, "hipMemcpy D2H");
@@ -745,9 +801,8 @@ edit_status_t edit_outer_state_set(edit_outer_t h, int32_t layer, const edit_lay
   Unit& u = h->units[layer];
   edit_status_t st = check_device(h);
   if (st != EDIT_OK) return st;
+  EDIT_TRY(wait_unit(h, u));
   hipError_t e = hipSuccess;
-  if (u.pending && (e = hipEventSynchronize(u.done)) != hipSuccess)
-    return fail_hip(e, "hipEventSynchronize");
   UnitRecord rec;
   if ((e = hipMemcpy(&rec, u.rec, sizeof rec, hipMemcpyDeviceToHost)) != hipSuccess)
     return fail_hip(e, "hipMemcpy D2H");
@@ -767,8 +822,7 @@ void edit_outer_destroy(edit_outer_t h) {
   if (!h) return;
   int prev = -1;
   if (hipGetDevice(&prev) == hipSuccess && prev != h->device) (void)hipSetDevice(h->device);
-  for (Unit& u : h->units)
-    if (u.pending) (void)hipEventSynchronize(u.done);
+  for (Unit& u : h->units) (void)wait_unit(h, u);
   destroy_units(h);
   if (prev >= 0 && prev != h->device) (void)hipSetDevice(prev);
   delete h;
