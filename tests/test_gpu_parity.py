@@ -281,6 +281,41 @@ def test_round_and_streams_match_unit_by_unit(K, dtype):
             assert x.round == y.round == 3
 
 
+def test_state_get_waits_for_its_round_through_the_event_ring():
+    """A round's units share one completion event from a small ring.  Seven
+    rounds are enqueued on two streams without any host synchronisation
+    (the ring wraps), then state_get is called at once: every unit must
+    report its last round, bit for bit as a handle that synchronised after
+    every round, and theta must match once the device is idle."""
+    sizes = [2_000_003, 1_500_000, 2_000_000, 1_000_001, 3_000_000, 750_007]
+    wl = synth.small("llama1b-k8-bf16", sizes, name="ring")
+    schedule = [(0, [0, 1])] + [(1, [2, 3]), (1, [4, 5])] * 3  # (stream, units)
+    results = []
+    for synced in (True, False):
+        h = EditOuter(OuterConfig(wl.num_workers, wl.layer_numel, "bf16", ema_warmup_rounds=1), DEV)
+        units = [_fresh_inputs(wl, u, 0, DEV) for u in range(wl.num_units)]
+        torch.cuda.synchronize()
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+        for si, us in schedule:
+            # later rounds of a unit see replicas equal to theta: zero pseudo gradients
+            streams[si].wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(streams[si]):
+                h.step_round([units[u] for u in us], layers=us)
+            if synced:
+                torch.cuda.synchronize()
+        states = [h.state_get(u) for u in range(wl.num_units)]  # no synchronisation before
+        torch.cuda.synchronize()
+        results.append(([tuple(t.clone() for t in (x[0], x[1])) for x in units], states))
+        h.close()
+    (ua, sa), (ub, sb) = results
+    expect_rounds = [1, 1, 3, 3, 3, 3]
+    for u in range(wl.num_units):
+        assert sa[u].round == sb[u].round == expect_rounds[u]
+        assert np.array_equal(sa[u].norm, sb[u].norm) and np.array_equal(sa[u].ema_mean, sb[u].ema_mean)
+        assert np.array_equal(sa[u].weight, sb[u].weight) and sa[u].clip_coef == sb[u].clip_coef
+        assert torch.equal(ua[u][0], ub[u][0]) and torch.equal(ua[u][1], ub[u][1])
+
+
 def test_round_rejects_repeated_unit():
     wl = synth.small("llama1b-k8-bf16", [4096, 4096], name="rep")
     h = EditOuter(OuterConfig(wl.num_workers, wl.layer_numel, "bf16"), DEV)
