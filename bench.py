@@ -31,7 +31,7 @@ METRIC = "outer-sync ms/step and achieved HBM GB/s (% of peak), 1B model K=8"
 DEFAULT_WORKLOAD = "llama1b-k8-bf16"  # 24 units x 51,384,320 elements, K = 8, bf16 replicas
 WORKLOAD_NAMES = ("linear1m-k4", "llama350m-k8-f32", "llama1b-k8-bf16", "llama7b-half-k8-bf16",
                   "aedit1b-k16-bf16", "paper1b-k8-bf16")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2412_07210_amd", "csrc", "edit_outer_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2412_07210_amd", "csrc")
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_counters.json")
 
 
@@ -50,8 +50,12 @@ def kernel_code_hash(text: str) -> str:
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SOURCE) as f:
-        return kernel_code_hash(f.read())
+    """The kernels file and the code fragments it includes."""
+    text = ""
+    for name in ["edit_outer_kernels.hip"] + sorted(f for f in os.listdir(CSRC) if f.endswith(".inc")):
+        with open(os.path.join(CSRC, name)) as f:
+            text += f.read()
+    return kernel_code_hash(text)
 
 
 def unit_bytes(n: int, K: int, R: int, active: int, rolled_back: bool, one_pass: bool = False) -> tuple:

@@ -49,6 +49,18 @@ struct DecideParams {
   uint32_t flags;
 };
 
+// A unit of a round whose Gram pass is a single block, stepped whole (Gram
+// row, decision, update) by one block of a small launch.
+constexpr int kMaxSingleBlockUnits = 4;  // per launch
+struct SingleBlockDesc {
+  float* theta;
+  float* mom;
+  void* const* reps;  // host array of K device pointers (read at launch)
+  double* partials;
+  UnitRecord* rec;
+  int64_t n;
+};
+
 // Launchers (kernels.hip).  All enqueue on `stream` and return the launch
 // status; none synchronises.
 // Pass 1 over `rows` partial rows; when prev_partials is not null, one more
@@ -58,6 +70,11 @@ hipError_t launch_pass1(int K, bool bf16, int rows, const float* theta,
                         const void* const* reps, int64_t n, double* partials,
                         const double* prev_partials, int prev_rows, UnitRecord* prev_rec,
                         const DecideParams& prm, hipStream_t stream);
+// A small launch of a round: the decision of a previous unit (when
+// prev_partials is not null) and `count` whole single-block units.
+hipError_t launch_round_small(int K, bool bf16, const double* prev_partials, int prev_rows,
+                              UnitRecord* prev_rec, const DecideParams& prm, const SingleBlockDesc* unit,
+                              int count, double lr, double rho, hipStream_t stream);
 hipError_t launch_decide(int K, const double* partials, int rows, UnitRecord* rec,
                          const DecideParams& prm, hipStream_t stream);
 // The fixed-order sum of the partials as a K(K+1)/2 vector in device memory.

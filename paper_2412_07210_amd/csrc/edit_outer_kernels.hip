@@ -395,60 +395,7 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_kernel(const fl
   }
   const int b = static_cast<int>(blockIdx.x) - first;  // this block's partial row
   const int rows = static_cast<int>(gridDim.x) - first;
-  // fp64 products and sums: on CDNA3/4 a v_fma_f64 issues at the rate of an
-  // unpacked v_fma_f32, so exactness costs no extra VALU cycles, and the
-  // Gram identity for ||sum_j w_j Delta_j|| stays accurate even when the
-  // workers' pseudo gradients nearly cancel.
-  double acc[NP];
-#pragma unroll
-  for (int p = 0; p < NP; ++p) acc[p] = 0.0;
-
-  const int64_t stride = static_cast<int64_t>(rows) * pass1_threads<K>();
-  int64_t v = static_cast<int64_t>(b) * pass1_threads<K>() + threadIdx.x;
-  // Double-buffered grid-stride loop: buffer A holds trip t, B trip t+1.
-  float thA[VE], thB[VE];
-  u32x4 rA[K], rB[K];
-  load_pass1<K, BF16, NT>(theta, reps, v, nvec, thA, rA);
-  while (v < nvec) {
-    load_pass1<K, BF16, NT>(theta, reps, v + stride, nvec, thB, rB);
-    gram_vector<K, BF16>(acc, rA, thA);
-    v += stride;
-    if (v >= nvec) break;
-    load_pass1<K, BF16, NT>(theta, reps, v + stride, nvec, thA, rA);
-    gram_vector<K, BF16>(acc, rB, thB);
-    v += stride;
-  }
-
-  // Ragged tail (fewer than VE elements past the last full vector): row 0.
-  const int64_t i = nvec * VE + threadIdx.x;
-  if (b == 0 && i < n) {
-    double d[K];
-    const double th = theta[i];
-#pragma unroll
-    for (int j = 0; j < K; ++j) d[j] = static_cast<double>(load_scalar<BF16>(reps.p[j], i)) - th;
-    int p = 0;
-#pragma unroll
-    for (int j = 0; j < K; ++j)
-#pragma unroll
-      for (int k = j; k < K; ++k, ++p) acc[p] = fma(d[j], d[k], acc[p]);
-  }
-
-  // Block reduction: wave butterfly, then the four waves in order.
-  __shared__ double red[pass1_threads<K>() / 64][NP];
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    const double s = wave_sum(acc[p]);
-    if (lane == 0) red[wave][p] = s;
-  }
-  __syncthreads();
-  for (int p = threadIdx.x; p < NP; p += pass1_threads<K>()) {
-    double s = red[0][p];
-#pragma unroll
-    for (int w = 1; w < pass1_threads<K>() / 64; ++w) s += red[w][p];
-    partials[static_cast<int64_t>(p) * rows + b] = s;
-  }
+#include "gram_rows_valu.inc"
 }
 
 // Pass 1 for 8 < K <= 16: the Gram matrix sum_i d_i d_i^T over the unit's
@@ -581,118 +528,7 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_mfma_kernel(con
   }
   const int b = static_cast<int>(blockIdx.x) - first;  // this block's partial row
   const int rows = static_cast<int>(gridDim.x) - first;
-  constexpr int NP = K * (K + 1) / 2;
-  constexpr int VE = Vec<BF16>::VE;
-  constexpr int G = Tiles4<K>::G;
-  constexpr int T = Tiles4<K>::T;
-  constexpr int kWaves = pass1_threads<K>() / 64;
-  // Vector slots per lane per group; a group is 16*V consecutive vectors of
-  // every worker, and one wave load instruction reads 256 contiguous bytes
-  // of each of four replicas.
-  constexpr int V = kMfmaSlots;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int c = lane & 3;
-  const int quad = lane >> 2;
-  const void* rep[G];
-  bool act[G];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const int w = 4 * g + c;
-    act[g] = w < K;
-    rep[g] = reps.p[4 * g];
-#pragma unroll
-    for (int j = 4 * g + 1; j < 4 * g + 4 && j < K; ++j) rep[g] = (w == j) ? reps.p[j] : rep[g];
-  }
-
-  const int64_t groups = (nvec + 16 * V - 1) / (16 * V);
-  const int64_t wave_stride = static_cast<int64_t>(rows) * kWaves;
-  auto load = [&](int64_t g, Quad4<G, BF16> (&q)[V]) {
-#pragma unroll
-    for (int u = 0; u < V; ++u) load_quad4<G, BF16, NT>(theta, rep, act, c, 16 * V * g + 16 * u + quad, nvec, q[u]);
-  };
-  auto accumulate = [&](double (&acc)[T], const Quad4<G, BF16> (&q)[V]) {
-#pragma unroll
-    for (int u = 0; u < V; ++u) gram_quad4_bcast<K, BF16>(acc, q[u], act);
-  };
-  double acc[T];
-#pragma unroll
-  for (int t = 0; t < T; ++t) acc[t] = 0.0;
-  int64_t g = static_cast<int64_t>(b) * kWaves + wave;
-  Quad4<G, BF16> qA[V], qB[V];
-  load(g, qA);
-  while (g < groups) {  // double-buffered like the VALU pass; wave-uniform
-    load(g + wave_stride, qB);
-    accumulate(acc, qA);
-    g += wave_stride;
-    if (g >= groups) break;
-    load(g + wave_stride, qA);
-    accumulate(acc, qB);
-    g += wave_stride;
-  }
-  // Ragged tail (fewer than VE elements past the last full vector): quad 0
-  // of row 0's first wave, element by element.  Wave-uniform, as the matrix
-  // instruction needs every lane.
-  if (b == 0 && wave == 0 && n > nvec * VE) {
-    u32x4 raw[G];
-    float th[VE];
-#pragma unroll
-    for (int g = 0; g < G; ++g) raw[g] = u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      const int64_t i = nvec * VE + e;
-      th[e] = (quad == 0 && i < n) ? theta[i] : 0.f;
-    }
-    if (quad == 0) {
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        if (!act[g]) continue;
-#pragma unroll
-        for (int e = 0; e < VE; ++e) {
-          const int64_t i = nvec * VE + e;
-          if (i < n) {
-            if constexpr (BF16) {
-              const uint32_t h = reinterpret_cast<const uint16_t*>(rep[g])[i];
-              raw[g][e >> 1] |= (e & 1) ? (h << 16) : h;
-            } else {
-              raw[g][e] = __float_as_uint(reinterpret_cast<const float*>(rep[g])[i]);
-            }
-          }
-        }
-      }
-    }
-    gram_quad4<K, BF16>(acc, raw, th, act);
-  }
-
-  // Block reduction: add the four instruction blocks (lanes l, l^4, l^8,
-  // l^12), write each wave's tiles to LDS, then the waves in order for each
-  // upper-triangle pair.
-  __shared__ double gsh[kWaves][16][16];
-  {
-    int t = 0;
-#pragma unroll
-    for (int I = 0; I < G; ++I)
-#pragma unroll
-      for (int J = I; J < G; ++J, ++t) {
-        double x = acc[t];
-        x += __shfl_xor(x, 4, 64);
-        x += __shfl_xor(x, 8, 64);
-        if ((quad & 3) == 0) gsh[wave][4 * I + (lane >> 4)][4 * J + c] = x;
-      }
-  }
-  __syncthreads();
-  for (int p = threadIdx.x; p < NP; p += pass1_threads<K>()) {
-    int j = 0, left = p;
-    while (left >= K - j) {
-      left -= K - j;
-      ++j;
-    }
-    const int k = j + left;
-    double s = gsh[0][j][k];
-#pragma unroll
-    for (int q = 1; q < kWaves; ++q) s += gsh[q][j][k];
-    partials[static_cast<int64_t>(p) * rows + b] = s;
-  }
+#include "gram_rows_mfma.inc"
 }
 // ---------------------------------------------------------------- decide
 
@@ -809,60 +645,91 @@ __global__ __launch_bounds__(kPass2Threads) void pass2_update_kernel(float* __re
   const int64_t tail = nvec * VE + threadIdx.x;
   const bool do_tail = blockIdx.x == 0 && tail < n;
 
-  if (rec->rollback) {  // every worker flagged: replicas <- theta_t, nothing else moves
-    if (v < nvec) {
-      float th[VE];
-      load_f32<VE, NT>(theta, v, th);
-      const u32x4 out = pack<BF16>(th);
+#include "update_vector_at.inc"
+}
+
+// ------------------------------------------- single-block units of a round
+
+// A unit whose Gram pass is one block (at most 256 vectors) can be stepped
+// whole by one block: its Gram row, the decision and the update pass, one
+// after the other.  A round does that for up to kMaxSingleBlockUnits such
+// units in one small launch, which may also carry the previous unit's
+// decision (round_small_kernel).  The block runs the code of the unit's own
+// three launches (pass 1 with one row, the decision, pass 2 with one vector
+// per thread), included from the same fragments, so the results are the
+// same bit for bit.  The partial row and the record are written and read
+// back within the block: __syncthreads() orders global memory between the
+// waves of one work-group (they share the CU's L1), and the record is read
+// with vector loads (it is written in this kernel).
+template <int K>
+struct SingleBlockUnit {
+  float* theta;
+  float* mom;
+  void* reps[K];
+  double* partials;
+  UnitRecord* rec;
+  int64_t n;
+};
+
+template <int K>
+struct SingleBlockUnits {
+  SingleBlockUnit<K> u[kMaxSingleBlockUnits];
+  int count;
+  double lr, rho;
+};
+
+template <int K, bool BF16, bool NT1, bool NT2, bool MFMA>
+__device__ void single_block_unit(const SingleBlockUnit<K>& su, const DecideParams& prm, double lr,
+                                  double rho) {
+  constexpr int VE = Vec<BF16>::VE;
+  const int64_t n = su.n;
+  const int64_t nvec = n / VE;
+  {  // pass 1: the unit's only Gram row
+    constexpr bool NT = NT1;
+    const float* __restrict__ theta = su.theta;
+    ConstPtrs<K> reps;
 #pragma unroll
-      for (int j = 0; j < K; ++j) st16<NT>(reinterpret_cast<u32x4*>(reps.p[j]) + v, out);
+    for (int j = 0; j < K; ++j) reps.p[j] = su.reps[j];
+    double* __restrict__ partials = su.partials;
+    const int b = 0, rows = 1;
+    if constexpr (MFMA) {
+#include "gram_rows_mfma.inc"
+    } else {
+      constexpr int NP = K * (K + 1) / 2;
+#include "gram_rows_valu.inc"
     }
-    if (do_tail) {
-      const float th = theta[tail];
+  }
+  __syncthreads();
+  run_prev_decide<K, pass1_threads<K>()>(PrevDecide{su.partials, 1, su.rec}, prm);
+  __syncthreads();
+  {  // pass 2: one vector per thread (nvec <= 256 <= the block's threads)
+    constexpr bool NT = NT2;
+    float* __restrict__ theta = su.theta;
+    float* __restrict__ mom = su.mom;
+    MutPtrs<K> reps;
 #pragma unroll
-      for (int j = 0; j < K; ++j) store_scalar<BF16>(reps.p[j], tail, th);
-    }
+    for (int j = 0; j < K; ++j) reps.p[j] = su.reps[j];
+    const UnitRecord* rec = su.rec;
+    const int64_t v = threadIdx.x;
+    const int64_t tail = nvec * VE + threadIdx.x;
+    const bool do_tail = tail < n;
+#include "update_vector_at.inc"
+  }
+}
+
+// Block 0 takes the previous unit's decision when prev.partials is set; one
+// block per single-block unit steps that unit.  The blocks have the pass-1
+// kernel's size, so a unit's Gram row is the one its own pass 1 would write.
+template <int K, bool BF16, bool NT1, bool NT2, bool MFMA>
+__global__ __launch_bounds__(pass1_threads<K>()) void round_small_kernel(PrevDecide prev, DecideParams prm,
+                                                               SingleBlockUnits<K> single) {
+  const int first = prev.partials ? 1 : 0;
+  if (first && blockIdx.x == 0) {
+    run_prev_decide<K, pass1_threads<K>()>(prev, prm);
     return;
   }
-
-  double c[K];
-  const u32x4* src[K];
-#pragma unroll
-  for (int j = 0; j < K; ++j) {
-    c[j] = rec->coef[j];
-    const int s = rec->src[j];
-    const void* ptr = reps.p[0];
-#pragma unroll
-    for (int i = 1; i < K; ++i) ptr = (s == i) ? reps.p[i] : ptr;
-    src[j] = reinterpret_cast<const u32x4*>(ptr);
-  }
-  const bool use = rec->use_deltas;
-
-  if (v < nvec) {
-    float th[VE], b[VE];
-    u32x4 raw[K];
-    load_pass2<K, BF16, NT>(theta, mom, src, use, v, nvec, th, b, raw);
-    update_vector<K, BF16, NT>(theta, mom, reps, c, use, v, th, b, raw, lr, rho);
-  }
-
-  if (do_tail) {
-    const float th = theta[tail];
-    double acc = 0.0;
-    if (use) {
-#pragma unroll
-      for (int j = 0; j < K; ++j)
-        acc = fma(c[j],
-                  static_cast<double>(load_scalar<BF16>(reinterpret_cast<const void*>(src[j]), tail)) -
-                      static_cast<double>(th),
-                  acc);
-    }
-    float tn, bn;
-    nesterov(acc, th, mom[tail], lr, rho, tn, bn);
-    theta[tail] = tn;
-    mom[tail] = bn;
-#pragma unroll
-    for (int j = 0; j < K; ++j) store_scalar<BF16>(reps.p[j], tail, tn);
-  }
+  const int sb = static_cast<int>(blockIdx.x) - first;
+  if (sb < single.count) single_block_unit<K, BF16, NT1, NT2, MFMA>(single.u[sb], prm, single.lr, single.rho);
 }
 
 // ------------------------------------------------------ one-pass mean step
@@ -1085,6 +952,32 @@ hipError_t pass1_launch(int rows, const float* theta, const void* const* reps, i
   return hipGetLastError();
 }
 
+template <int K, bool BF16>
+hipError_t round_small_launch(const double* prev_partials, int prev_rows, UnitRecord* prev_rec,
+                              const DecideParams& prm, const SingleBlockDesc* unit, int count, double lr,
+                              double rho, hipStream_t stream) {
+  const PrevDecide prev{prev_partials, prev_rows, prev_rec};
+  SingleBlockUnits<K> single{};
+  single.count = count;
+  single.lr = lr;
+  single.rho = rho;
+  for (int i = 0; i < count; ++i) {
+    const SingleBlockDesc& d = unit[i];
+    single.u[i].theta = d.theta;
+    single.u[i].mom = d.mom;
+    for (int j = 0; j < K; ++j) single.u[i].reps[j] = d.n > 0 ? d.reps[j] : nullptr;
+    single.u[i].partials = d.partials;
+    single.u[i].rec = d.rec;
+    single.u[i].n = d.n;
+  }
+  const int blocks = (prev_partials ? 1 : 0) + count;
+  if (blocks == 0) return hipSuccess;
+  constexpr bool kMfma = K > 8;
+  hipLaunchKernelGGL((round_small_kernel<K, BF16, kMfma ? kNTMfma : kNT1, kNT2, kMfma>), dim3(blocks),
+                     dim3(pass1_threads<K>()), 0, stream, prev, prm, single);
+  return hipGetLastError();
+}
+
 template <int K>
 hipError_t decide_launch(const double* partials, int rows, UnitRecord* rec, const DecideParams& prm,
                          hipStream_t stream) {
@@ -1166,6 +1059,24 @@ hipError_t launch_pass1(int K, bool bf16, int rows, const float* theta, const vo
                                          prev_rows, prev_rec, prm, stream)                  \
                 : pass1_launch<KK, false>(rows, theta, reps, n, partials, prev_partials,    \
                                           prev_rows, prev_rec, prm, stream);
+    EDIT_FOR_EACH_K(EDIT_CASE)
+#undef EDIT_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_round_small(int K, bool bf16, const double* prev_partials, int prev_rows,
+                              UnitRecord* prev_rec, const DecideParams& prm, const SingleBlockDesc* unit,
+                              int count, double lr, double rho, hipStream_t stream) {
+  if (count < 0 || count > kMaxSingleBlockUnits) return hipErrorInvalidValue;
+  switch (K) {
+#define EDIT_CASE(KK)                                                                              \
+  case KK:                                                                                         \
+    return bf16 ? round_small_launch<KK, true>(prev_partials, prev_rows, prev_rec, prm, unit, count, \
+                                               lr, rho, stream)                                    \
+                : round_small_launch<KK, false>(prev_partials, prev_rows, prev_rec, prm, unit,     \
+                                                count, lr, rho, stream);
     EDIT_FOR_EACH_K(EDIT_CASE)
 #undef EDIT_CASE
     default:

@@ -402,6 +402,14 @@ struct Enqueue {
                                 prev ? prev->rec : nullptr, prm, s);
     return e == hipSuccess ? EDIT_OK : fail_hip(e, "pass1 launch");
   }
+  // a small launch: the decision of `prev` (may be null) and whole
+  // single-block units
+  edit_status_t small(Unit* prev, const SingleBlockDesc* single, int nsingle) {
+    hipError_t e = launch_round_small(K, bf16, prev ? prev->partials : nullptr, prev ? prev->rows : 0,
+                                      prev ? prev->rec : nullptr, prm, single, nsingle,
+                                      h->cfg.outer_lr, h->cfg.momentum, s);
+    return e == hipSuccess ? EDIT_OK : fail_hip(e, "small launch");
+  }
   edit_status_t gram_out(int32_t layer, double* gram) {
     Unit& u = h->units[layer];
     hipError_t e = launch_gram_reduce(K, u.partials, u.rows, gram, s);
@@ -589,13 +597,26 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
     EDIT_TRY(q.records(0, h->cfg.num_layers));
     return q.finish_round(layers, count);
   }
-  // Every unit's decision rides in the next unit's pass-1 launch (one extra
-  // block, which would otherwise idle), and its pass 2 follows that launch;
-  // only the round's last decision runs as a kernel of its own.  The one-block
-  // decision then never holds up the whole chip (measured at the 1B shape,
-  // same box: 14.63-14.68 ms per round against 14.79 ms with a decision
-  // kernel between each unit's two passes).
+  // Up to K = 8 every unit's decision rides in the next unit's pass-1 launch
+  // (one extra block, which would otherwise idle), and its pass 2 follows
+  // that launch; the one-block decision then never holds up the whole chip
+  // (measured at the 1B shape, same box: 14.63-14.68 ms per round against
+  // 14.79 ms with a decision kernel between each unit's two passes).  Above
+  // K = 8 the Gram pass is bound by fp64 arithmetic and reads through the
+  // cache, so a unit's pass 2 instead follows its own pass 1 with only the
+  // decision between them and finds the end of its input in the Infinity
+  // Cache (measured at K = 16: 696 against 730 us per 51.4M-element pass 2).
+  //
+  // A unit whose Gram pass is one block is stepped whole by one block of a
+  // small launch, up to kMaxSingleBlockUnits per launch (its own two
+  // launches cost about 16 us at K = 16, its work a few microseconds); a
+  // small launch also carries the pending decision.  Such units are
+  // independent of the others, so this only changes which launch runs them.
+  // Units whose kernels are being timed keep their own launches.
+  const bool adjacent = K > 8;
   int32_t pending = -1;  // index i of the unit whose decision is not launched yet
+  SingleBlockDesc single[kMaxSingleBlockUnits];
+  int nsingle = 0;
   auto flush_pass2 = [&](int32_t i) -> edit_status_t {
     const int32_t l = layers[i];
     void* const* reps = replicas + static_cast<size_t>(i) * K;
@@ -603,9 +624,31 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
     EDIT_TRY(q.pass2(l, theta[i], momentum[i], reps));
     return q.event(h->units[l], l, 3);
   };
+  // the pending decision (if any) and the waiting single-block units, then
+  // the pending unit's pass 2
+  auto flush_small = [&]() -> edit_status_t {
+    EDIT_TRY(q.small(pending >= 0 ? &h->units[layers[pending]] : nullptr, single, nsingle));
+    nsingle = 0;
+    if (pending >= 0) EDIT_TRY(flush_pass2(pending));
+    pending = -1;
+    return EDIT_OK;
+  };
   for (int32_t i = 0; i < count; ++i) {
     const int32_t l = layers[i];
     Unit& u = h->units[l];
+    if (u.rows == 1 && !q.profiled(l)) {
+      single[nsingle++] = {theta[i], momentum[i], replicas + static_cast<size_t>(i) * K, u.partials,
+                           u.rec, u.n};
+      if (nsingle == kMaxSingleBlockUnits) EDIT_TRY(flush_small());
+      continue;
+    }
+    if (nsingle > 0) {
+      EDIT_TRY(flush_small());
+    } else if (adjacent && pending >= 0) {
+      EDIT_TRY(q.decide(layers[pending]));
+      EDIT_TRY(flush_pass2(pending));
+      pending = -1;
+    }
     Unit* prev = pending >= 0 ? &h->units[layers[pending]] : nullptr;
     EDIT_TRY(q.event(u, l, 0));
     EDIT_TRY(q.pass1(l, theta[i], replicas + static_cast<size_t>(i) * K, prev));
@@ -613,7 +656,9 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
     if (pending >= 0) EDIT_TRY(flush_pass2(pending));
     pending = i;
   }
-  if (pending >= 0) {
+  if (nsingle > 0) {
+    EDIT_TRY(flush_small());
+  } else if (pending >= 0) {
     EDIT_TRY(q.decide(layers[pending]));
     EDIT_TRY(flush_pass2(pending));
   }
@@ -856,12 +901,14 @@ edit_status_t edit_outer_copy_probe(void* dst, const void* src, int64_t nbytes, 
     return fail(EDIT_EINVAL, "dst and src must be non-NULL and 16-byte aligned");
   const uintptr_t d = reinterpret_cast<uintptr_t>(dst), s = reinterpret_cast<uintptr_t>(src);
   if (d < s + nbytes && s < d + nbytes) return fail(EDIT_EINVAL, "dst and src overlap");
-  int dev = 0, cus = 0;
+  int dev = 0;
   hipError_t e = hipGetDevice(&dev);
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e != hipSuccess) return fail_hip(e, "device query");
+  if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+  // One 16-byte vector per thread, a flat grid, as in the update pass (a
+  // persistent grid-stride copy measured 4.6 TB/s against 6.2 here); the
+  // grid-stride loop only takes over past the largest grid.
   const int64_t nvec = nbytes / 16;
-  const int blocks = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(int64_t(cus) * 8, ceil_div(nvec, kThreads))));
+  const int blocks = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(INT32_MAX, ceil_div(nvec, kThreads))));
   e = launch_copy(dst, src, nbytes, blocks, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail_hip(e, "copy launch");
   return EDIT_OK;

@@ -172,20 +172,40 @@ class ParityRun:
                 self.lib.state_set(self.index[u], mu, sig, r)
             self.cases.append(case)
 
-    def round(self, t: int, std: Optional[np.ndarray] = None, poison: Optional[dict] = None,
-              verbose: bool = False) -> List[dict]:
-        """One outer round on every selected unit; returns the oracle records."""
-        out = []
-        for c in self.cases:
-            t0 = time.time()
-            c.theta_d.copy_(torch.from_numpy(c.theta_h))
-            c.mom_d.copy_(torch.from_numpy(c.mom_h))
-            self.wl.fill_replicas(c.theta_d, c.reps_d, c.unit, t, self.seed, std=std)
-            if poison:
-                for j, (idx, val) in poison.items():
+    def _inputs(self, c: UnitCase, t: int, std, poison) -> List[np.ndarray]:
+        c.theta_d.copy_(torch.from_numpy(c.theta_h))
+        c.mom_d.copy_(torch.from_numpy(c.mom_h))
+        self.wl.fill_replicas(c.theta_d, c.reps_d, c.unit, t, self.seed, std=std)
+        if poison:
+            for j, (idx, val) in poison.items():
+                if idx < c.theta_d.numel():  # entries past a unit's end are skipped
                     c.reps_d[j][idx] = val
-            reps_h = [host_bits(r) for r in c.reps_d]
-            self.lib.step_layer(self.index[c.unit], c.theta_d, c.mom_d, c.reps_d)
+        return [host_bits(r) for r in c.reps_d]
+
+    def round(self, t: int, std: Optional[np.ndarray] = None, poison: Optional[dict] = None,
+              verbose: bool = False, via_round: bool = False,
+              order: Optional[Sequence[int]] = None) -> List[dict]:
+        """One outer round on every selected unit; returns the oracle records.
+
+        By default each unit is one edit_outer_step_layer call.  With
+        via_round, every unit's inputs are made first and the whole round is
+        one edit_outer_step_round call over the cases in `order` (indices into
+        the selected units; default: as selected)."""
+        out = []
+        reps_all = None
+        if via_round:
+            reps_all = [self._inputs(c, t, std, poison) for c in self.cases]
+            seq = list(range(len(self.cases))) if order is None else list(order)
+            sel = [self.cases[i] for i in seq]
+            self.lib.step_round([(c.theta_d, c.mom_d, c.reps_d) for c in sel],
+                                layers=[self.index[c.unit] for c in sel])
+        for ci, c in enumerate(self.cases):
+            t0 = time.time()
+            if via_round:
+                reps_h = reps_all[ci]
+            else:
+                reps_h = self._inputs(c, t, std, poison)
+                self.lib.step_layer(self.index[c.unit], c.theta_d, c.mom_d, c.reps_d)
             rec = c.oracle.step(c.theta_h, c.mom_h, reps_h)
             torch.cuda.synchronize(self.device)
             what = f"{self.wl.name} unit {c.unit} round {t}"

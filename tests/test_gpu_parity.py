@@ -281,6 +281,82 @@ def test_round_and_streams_match_unit_by_unit(K, dtype):
             assert x.round == y.round == 3
 
 
+# Units whose Gram pass is one block (at most 256 vectors: 2,048 bf16 or
+# 1,024 fp32 elements) ride whole in another unit's pass-1 launch, up to four
+# per launch.  The sizes put six of them first (a launch of riders only, then
+# two riding with the first large unit), one and two between large units,
+# and five at the end (a riders-only launch carrying the last large unit's
+# decision).
+_SINGLE_BLOCK_SIZES = {
+    "bf16": [0, 1, 7, 8, 2048, 2049, 300_001, 9, 65_537, 255, 2041, 1_000_003, 5, 2047, 16, 3, 2048],
+    "f32": [0, 1, 7, 8, 1024, 1027, 300_001, 9, 65_537, 255, 1021, 1_000_003, 5, 1023, 16, 3, 1024],
+}
+
+
+@pytest.mark.parametrize("K,dtype", [(1, "bf16"), (3, "f32"), (8, "bf16"), (8, "f32"), (9, "bf16"),
+                                     (16, "bf16"), (16, "f32")])
+def test_single_block_units_in_a_round_match_the_oracle(K, dtype):
+    """A round dense in single-block units, stepped by edit_outer_step_round,
+    against the oracle: a x40 worker in round 3, every worker x1000 in round 4
+    (all flagged: rollback), a NaN replica in round 5."""
+    sizes = _SINGLE_BLOCK_SIZES[dtype]
+    ve = 8 if dtype == "bf16" else 4
+    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=2,
+                     clip_threshold=0.05, name=f"single{K}{dtype}")
+    run = ParityRun(wl, range(len(sizes)), DEV)
+    order = [int(i) for i in np.random.default_rng(K).permutation(len(sizes))] if K == 8 else None
+    try:
+        for t in range(6):
+            std = wl.worker_std(t)
+            if t == 3:
+                std = std * np.where(np.arange(K) == K - 1, 40.0, 1.0)
+            if t == 4:
+                std = std * 1000.0
+            poison = {0: (0, float("nan"))} if t == 5 else None
+            recs = run.round(t, std=std, poison=poison, via_round=True, order=order)
+            if t == 4:  # the rollback path ran in some single-block unit
+                assert any(r["rolled_back"] for n, r in zip(sizes, recs) if 64 <= n <= 256 * ve)
+    except NearTie as e:
+        pytest.skip(str(e))
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("K,dtype", [(2, "bf16"), (8, "bf16"), (8, "f32"), (16, "bf16")])
+def test_single_block_units_in_a_round_match_unit_by_unit(K, dtype):
+    """The same round with single-block units riding in pass-1 launches gives
+    the bits of unit-by-unit edit_outer_step_layer calls, over three rounds."""
+    sizes = _SINGLE_BLOCK_SIZES[dtype]
+    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=1,
+                     name=f"singlebits{K}{dtype}")
+    order = [int(i) for i in np.random.default_rng(7).permutation(len(sizes))]
+    results = []
+    for mode in ("layer", "round"):
+        h = EditOuter(OuterConfig(K, wl.layer_numel, dtype, ema_warmup_rounds=1), DEV)
+        units = [_fresh_inputs(wl, u, 0, DEV) for u in range(wl.num_units)]
+        for t in range(3):
+            for u in range(wl.num_units):
+                wl.fill_replicas(units[u][0], units[u][2], u, t)
+            torch.cuda.synchronize()
+            if mode == "layer":
+                for u in order:
+                    h.step_layer(u, *units[u])
+            else:
+                h.step_round([units[u] for u in order], layers=order)
+            torch.cuda.synchronize()
+        results.append((units, [h.state_get(u) for u in range(wl.num_units)]))
+        h.close()
+    (ua, sa), (ub, sb) = results
+    for u, (a, b) in enumerate(zip(ua, ub)):
+        assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1]), f"unit {u}"
+        assert all(torch.equal(x, y) for x, y in zip(a[2], b[2])), f"unit {u}"
+    for x, y in zip(sa, sb):
+        for f in ("norm", "ema_mean", "ema_std", "weight", "anomalous"):
+            assert np.array_equal(getattr(x, f), getattr(y, f)), f
+        assert x.synced_norm == y.synced_norm and x.clip_coef == y.clip_coef
+        assert x.round == y.round == 3
+
+
 def test_state_get_waits_for_its_round_through_the_event_ring():
     """A round's units share one completion event from a small ring.  Seven
     rounds are enqueued on two streams without any host synchronisation
