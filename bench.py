@@ -198,7 +198,7 @@ SHORT = {"pass1_gram_kernel": "pass1", "decide_kernel": "decide", "pass2_update_
 
 def _kernel_kind(name: str) -> str:
     for kind in ("pass1_gram_kernel", "pass1_gram_mfma_kernel", "decide_kernel", "pass2_update_kernel",
-                 "fused_mean_kernel", "fused_finish_kernel", "copy_kernel"):
+                 "round_small_kernel", "fused_mean_kernel", "fused_finish_kernel", "copy_kernel"):
         if kind in name:
             return kind
     return ""
@@ -236,7 +236,7 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
             nvec = -(-n // ve)
             if kind == "pass2_update_kernel" and -(-nvec // 128) * 128 == grid:
                 return n
-            tpb = 768 if kind == "pass1_gram_mfma_kernel" else 512  # threads per Gram-pass block
+            tpb = 768 if kind == "pass1_gram_mfma_kernel" else 256  # threads per Gram-pass block
             if kind.startswith("pass1_gram") and -(-nvec // 256) >= grid // tpb - 1:
                 return n
         return None
@@ -263,7 +263,7 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
     # method (the stream's dependency latency; torch and copy kernels excluded)
     spans.sort()
     ours = {"pass1_gram_kernel", "pass1_gram_mfma_kernel", "decide_kernel", "pass2_update_kernel",
-            "fused_mean_kernel", "fused_finish_kernel"}
+            "round_small_kernel", "fused_mean_kernel", "fused_finish_kernel"}
     pairs = [(a[2], b[2], b[0] - a[1]) for a, b in zip(spans, spans[1:]) if a[2] in ours and b[2] in ours]
     gaps = sorted(g for _, _, g in pairs)
     if gaps:
