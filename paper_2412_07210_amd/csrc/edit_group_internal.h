@@ -10,7 +10,8 @@
 
 namespace edit {
 
-constexpr int kGroupThreads = 256;        // persistent streaming passes
+constexpr int kGroupThreads = 256;        // streaming passes
+constexpr int kGroupNormVecs = 2;        // 16-byte vectors per thread of the norm pass
 constexpr int kGroupUpdateThreads = 128;  // the update pass
 constexpr int kGroupOneBlock = 1024;      // the one-block reductions
 
@@ -52,7 +53,6 @@ hipError_t launch_group_clip(const double* partials, int rows, GroupRecord* rec,
 hipError_t launch_group_update(bool bf16, int blocks, const GroupRecord* rec, const float* dbar,
                                float* theta, float* mom, void* rep, int64_t n, double lr, double rho,
                                hipStream_t stream);
-int group_norm_blocks_per_cu(bool bf16);
 int group_dbar_blocks_per_cu();
 
 // Shared with the single-GPU runtime (edit_outer_runtime.hip): the calling

@@ -181,8 +181,12 @@ __device__ __forceinline__ void gnorm_vector(float* delta, int64_t v, int64_t nv
   gstore_f32<VE, NT>(delta, v, out);
 }
 
-// Persistent grid of `rows` blocks: grid-stride over the vectors, each lane
-// double-buffered (the loads of trip t+1 in flight while trip t is summed).
+// A flat grid: each block owns kGroupNormVecs * kGroupThreads consecutive
+// vectors, a thread loads its kGroupNormVecs vectors before computing, and
+// the block leaves one partial sum of squares.  The pass writes 4 of every
+// 10 bytes it moves (the fp32 export at bf16); with writes in the traffic a
+// flat grid keeps the streams' in-flight window short and ordered (the
+// update pass measured the same).
 template <bool BF16, bool NT>
 __global__ __launch_bounds__(kGroupThreads) void group_norm_kernel(const float* __restrict__ theta,
                                                                   const void* __restrict__ rep,
@@ -190,21 +194,17 @@ __global__ __launch_bounds__(kGroupThreads) void group_norm_kernel(const float* 
                                                                   int64_t nvec, int64_t n,
                                                                   double* __restrict__ partials) {
   constexpr int VE = GVec<BF16>::VE;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kGroupThreads;
-  int64_t v = static_cast<int64_t>(blockIdx.x) * kGroupThreads + threadIdx.x;
-  double acc = 0.0;
-  float thA[VE], thB[VE];
-  u32x4 rA = {0u, 0u, 0u, 0u}, rB = {0u, 0u, 0u, 0u};
-  gnorm_load<BF16, NT>(theta, rep, v, nvec, thA, rA);
-  while (v < nvec) {
-    gnorm_load<BF16, NT>(theta, rep, v + stride, nvec, thB, rB);
-    gnorm_vector<BF16, NT>(delta, v, nvec, thA, rA, acc);
-    v += stride;
-    if (v >= nvec) break;
-    gnorm_load<BF16, NT>(theta, rep, v + stride, nvec, thA, rA);
-    gnorm_vector<BF16, NT>(delta, v, nvec, thB, rB, acc);
-    v += stride;
+  const int64_t v0 = static_cast<int64_t>(blockIdx.x) * (kGroupThreads * kGroupNormVecs) + threadIdx.x;
+  float th[kGroupNormVecs][VE];
+  u32x4 raw[kGroupNormVecs];
+#pragma unroll
+  for (int u = 0; u < kGroupNormVecs; ++u) {
+    raw[u] = u32x4{0u, 0u, 0u, 0u};
+    gnorm_load<BF16, NT>(theta, rep, v0 + u * kGroupThreads, nvec, th[u], raw[u]);
   }
+  double acc = 0.0;
+#pragma unroll
+  for (int u = 0; u < kGroupNormVecs; ++u) gnorm_vector<BF16, NT>(delta, v0 + u * kGroupThreads, nvec, th[u], raw[u], acc);
   const int64_t i = nvec * VE + threadIdx.x;  // ragged tail: block 0
   if (blockIdx.x == 0 && i < n) {
     const double d = static_cast<double>(gscalar<BF16>(rep, i)) - static_cast<double>(theta[i]);
@@ -457,10 +457,6 @@ hipError_t launch_group_update(bool bf16, int blocks, const GroupRecord* rec, co
   return hipGetLastError();
 }
 
-int group_norm_blocks_per_cu(bool bf16) {
-  return bf16 ? gocc(group_norm_kernel<true, kGroupNT>, kGroupThreads)
-              : gocc(group_norm_kernel<false, kGroupNT>, kGroupThreads);
-}
 
 int group_dbar_blocks_per_cu() { return gocc(group_dbar_kernel<kGroupNT>, kGroupThreads); }
 

@@ -181,7 +181,6 @@ edit_status_t edit_group_init(const edit_outer_config_t* cfg, int32_t rank, edit
   h->device = dev;
   const bool bf16 = cfg->replica_dtype == EDIT_BF16;
   const int ve = bf16 ? 8 : 4;
-  const int cap_norm = num_cu * group_norm_blocks_per_cu(bf16);
   const int cap_dbar = num_cu * group_dbar_blocks_per_cu();
 
   const size_t rec_bytes = (sizeof(GroupRecord) + 255) & ~size_t(255);
@@ -196,7 +195,7 @@ edit_status_t edit_group_init(const edit_outer_config_t* cfg, int32_t rank, edit
       delete h;
       return gfail(EDIT_EINVAL, "layer_numel[" + std::to_string(l) + "] is too large");
     }
-    u.rows_norm = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(cap_norm, gceil_div(nvec, kGroupThreads))));
+    u.rows_norm = static_cast<int>(std::max<int64_t>(1, gceil_div(nvec, int64_t(kGroupThreads) * kGroupNormVecs)));
     u.rows_dbar = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(cap_dbar, gceil_div(u.n / 4, kGroupThreads))));
     u.blocks_up = static_cast<int>(std::max<int64_t>(1, gceil_div(nvec, kGroupUpdateThreads)));
     u.blocks_clear = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(num_cu, gceil_div(u.n / 4, kGroupThreads))));
