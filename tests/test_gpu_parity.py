@@ -1,9 +1,9 @@
 """GPU parity of the HIP outer step against the CPU oracle (needs an MI355X).
 
 Small cases span several 256-thread blocks and ragged tails; full-size
-cases run single units of each workload at their real shapes, through a
-handle configured with every unit of the workload, i.e. the launch
-configuration the benchmark times.
+cases run units of each workload at their real shapes, through a handle
+configured with every unit of the workload and stepped by
+edit_outer_step_round, i.e. the launch configuration the benchmark times.
 """
 import math
 
@@ -47,7 +47,7 @@ def test_linear1m_k4_all_rounds():
     """1024x1024 fp32, K = 4: ten clean rounds, then worker 3 x50 is masked."""
     wl = synth.get("linear1m-k4")
     run = ParityRun(wl, [0], DEV)
-    recs = _run(run, range(11))
+    recs = _run(run, range(11), via_round=True)
     assert [int(x) for x in recs[10][0]["anomalous"]] == [0, 0, 0, 1]
     assert all(not r[0]["anomalous"].any() for r in recs[:10])
     assert recs[10][0]["clip_coef"] == 1.0
@@ -138,16 +138,19 @@ def test_llama350m_f32_full_units():
     wl = synth.get("llama350m-k8-f32")
     units = [0, 23]
     run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 10) for u in units})
-    _run(run, [10, 11])
+    _run(run, [10, 11], via_round=True)
 
 
-def test_llama1b_bf16_full_units_with_anomaly():
+@pytest.mark.parametrize("entry", ["round", "layer"])
+def test_llama1b_bf16_full_units_with_anomaly(entry):
     """Llama-1B-shaped units (51,384,320 elements, bf16 replicas, K = 8),
-    rounds 18-19: round 19 has one worker x20, which must be masked."""
+    rounds 18-19: round 19 has one worker x20, which must be masked.  Stepped
+    as one round (unit 0's decision inside unit 11's pass-1 launch) and unit
+    by unit."""
     wl = synth.get("llama1b-k8-bf16")
     units = [0, 11]
     run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 18) for u in units})
-    recs = _run(run, [18, 19])
+    recs = _run(run, [18, 19], via_round=entry == "round")
     bad = list(wl.anomalies(19).keys())[0]
     for r in recs[1]:
         assert r["anomalous"][bad] == 1
@@ -160,7 +163,7 @@ def test_paper1b_full_units_with_anomaly():
     assert wl.unit_numel(0) == 28_314_624 and wl.num_units == 32
     units = [0, 31]
     run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 19) for u in units})
-    recs = _run(run, [19])
+    recs = _run(run, [19], via_round=True)
     bad = list(wl.anomalies(19).keys())[0]
     for r in recs[0]:
         assert r["anomalous"][bad] == 1 and r["anomalous"].sum() == 1
@@ -170,17 +173,19 @@ def test_llama7b_half_full_unit_clip_active():
     """7B half shard (101,191,680 elements, bf16, K = 8) with phi = 0.889: clipping active."""
     wl = synth.get("llama7b-half-k8-bf16")
     run = ParityRun(wl, [5], DEV, ema_state={5: _expected_ema(wl, 5, 10)})
-    recs = _run(run, [10])
+    recs = _run(run, [10], via_round=True)
     assert recs[0][0]["clip_coef"] < 1.0
 
 
 def test_aedit1b_k16_full_layer():
     """A-EDiT round on 1B shapes, K = 16: one layer's matrix unit (51,380,224)
-    and its two 2,048-element RMSNorm units, three workers x30."""
+    and its two 2,048-element RMSNorm units, three workers x30.  As one round:
+    the gains are stepped whole in the small launch that takes the matrix
+    unit's decision."""
     wl = synth.get("aedit1b-k16-bf16")
     units = [0, 1, 2]
     run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 10) for u in units})
-    recs = _run(run, [10])
+    recs = _run(run, [10], via_round=True)
     flagged = sorted(wl.anomalies(10).keys())
     for r in recs[0]:
         assert sorted(np.flatnonzero(r["anomalous"]).tolist()) == flagged
