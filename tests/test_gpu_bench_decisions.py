@@ -1,19 +1,22 @@
-"""The benchmark workload's decisions, every unit and every round, against the
+"""Every workload's decisions, every unit and every round, against the
 oracle's decision on the library's own Gram matrices.
 
-The 1B K = 8 bf16 workload (24 units of 51,384,320 elements) is stepped with
-edit_outer_step_round, the call the benchmark times, for the benchmark's
-100 rounds with its seeds (so these are the decisions of a default benchmark
-run): ten warm-up rounds of the EMA state (Sec. 3.2), then z-tested rounds in
-which the per-worker pseudo-gradient scales vary (so workers are also
-flagged on their own), with one worker x20 in rounds 19, 29, ..., 99.
+Each workload is stepped with edit_outer_step_round, the call the benchmark
+times, with the benchmark's seeds: the 1B K = 8 bf16 workload (24 units of
+51,384,320 elements) for the benchmark's 100 rounds (so these are the
+decisions of a default benchmark run), the others for their warm-up and ten
+to twenty more rounds.  The EMA state warms up first (Sec. 3.2); then rounds
+are z-tested, the per-worker pseudo-gradient scales vary (so workers are
+also flagged on their own), and the injected workers are scaled up (1B:
+one worker x20 in rounds 19, 29, ..., 99; A-EDiT: three workers x30).
 Before each round every unit's Gram matrix is exported with
 edit_outer_gram_layer, which reduces the same partial sums in the same order
-as the step, so it is the matrix the step decides on.  The oracle takes its decision from that matrix
-(oracle_decide_gram), carrying its own EMA state from round to round, and
-the library's record must agree: the mask exactly, the round counter,
-rollback and z-test flags, and the norms, weights, EMA state, Gbar and beta
-to 1e-13 relative.
+as the step, so it is the matrix the step decides on (also for the A-EDiT
+gains, stepped whole in small launches).  The oracle takes its decision from
+that matrix (oracle_decide_gram), carrying its own EMA state from round to
+round, and the library's record must agree: the mask exactly, the round
+counter, rollback and z-test flags, and the norms, weights, EMA state, Gbar
+and beta to 1e-13 relative.
 """
 import numpy as np
 import pytest
@@ -25,7 +28,6 @@ from paper_2412_07210_amd import EditOuter, OuterConfig, synth
 pytestmark = pytest.mark.gpu
 
 DEV = torch.device("cuda:0")
-ROUNDS = 100  # the benchmark's default warm-up + timed rounds
 RTOL = 1e-13
 TIE = 1e-12  # z-test margins this close to a tie may round either way
 
@@ -37,8 +39,22 @@ def _close(lib, ref, what):
     assert ok.all(), f"{what}: library {lib} oracle {ref}"
 
 
-def test_every_decision_of_the_1b_workload():
-    wl = synth.get("llama1b-k8-bf16")
+# workload -> rounds (the 1B workload: the benchmark's default 10 warm-up + 90 timed)
+WORKLOAD_ROUNDS = {
+    "llama1b-k8-bf16": 100,
+    "linear1m-k4": 11,
+    "llama350m-k8-f32": 30,
+    "paper1b-k8-bf16": 30,
+    "llama7b-half-k8-bf16": 20,
+    "aedit1b-k16-bf16": 20,
+}
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name", list(WORKLOAD_ROUNDS))
+def test_every_decision_of_the_workload(name):
+    ROUNDS = WORKLOAD_ROUNDS[name]
+    wl = synth.get(name)
     K, L = wl.num_workers, wl.num_units
     hyper = wl.hyper()
     warm = hyper.pop("warmup_rounds")
@@ -53,7 +69,7 @@ def test_every_decision_of_the_1b_workload():
                           [torch.empty(th.numel(), dtype=wl.torch_dtype, device=DEV) for _ in range(K)]))
         grams = torch.empty(L, lib.num_pairs, dtype=torch.float64, device=DEV)
         plan = lib.prepare_round(units)
-        masked = 0
+        masked = boosted_flags = clipped = 0
         for t in range(ROUNDS):
             std = wl.worker_std(t)
             for u, (th, _, reps) in enumerate(units):
@@ -84,11 +100,18 @@ def test_every_decision_of_the_1b_workload():
                 if not rec["rolled_back"]:
                     _close(st.synced_norm, rec["synced_norm"], what + ": Gbar")
                     _close(st.clip_coef, rec["clip_coef"], what + ": beta")
-                for j in boosted:  # a x20 worker fails the z-test in every unit
-                    assert mask_o[j] == 1, f"{what}: boosted worker {j} not flagged"
+                if t >= warm:
+                    for j in boosted:  # a scaled-up worker fails the z-test in every unit
+                        assert mask_o[j] == 1, f"{what}: boosted worker {j} not flagged"
+                    boosted_flags += len(boosted)
                 masked += int(mask_o.sum())
-            print(f"  round {t}: {L} units agree, boosted {sorted(boosted)}, masked so far {masked}",
-                  flush=True)
-        assert masked > 9 * L  # the boosted rounds alone flag 9L workers
+                clipped += int(not rec["rolled_back"] and rec["clip_coef"] < 1.0)
+            print(f"  {name} round {t}: {L} units agree, boosted {sorted(boosted)}, masked so far "
+                  f"{masked}, clipped so far {clipped}", flush=True)
+        assert masked >= boosted_flags
+        if name == "llama1b-k8-bf16":
+            assert boosted_flags == 9 * L  # rounds 19, 29, ..., 99
+        if name == "llama7b-half-k8-bf16":  # phi = 0.889 clips every unit (see synth)
+            assert clipped == ROUNDS * L
     finally:
         lib.close()
