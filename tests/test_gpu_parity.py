@@ -141,6 +141,15 @@ def test_llama350m_f32_full_units():
     _run(run, [10, 11], via_round=True)
 
 
+def test_llama350m_f32_every_unit_of_a_round():
+    """All 24 units of the 350M workload in one full-size round, every element
+    of theta, b and the replicas against the oracle."""
+    wl = synth.get("llama350m-k8-f32")
+    units = list(range(wl.num_units))
+    run = ParityRun(wl, units, DEV, ema_state={u: _expected_ema(wl, u, 10) for u in units})
+    _run(run, [10], verbose=False, via_round=True)
+
+
 @pytest.mark.parametrize("entry", ["round", "layer"])
 def test_llama1b_bf16_full_units_with_anomaly(entry):
     """Llama-1B-shaped units (51,384,320 elements, bf16 replicas, K = 8),
