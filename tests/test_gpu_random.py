@@ -4,8 +4,10 @@ Each case draws K, unit sizes, the replica type, the penalty switches
 (sometimes the one-pass mode), the hyper-parameters (including edge values:
 rho = 0, alpha = 1, delta = 0, phi = 0, a one-round warm-up) and per-round
 worker scales with occasional x30 or x1000 workers, then steps library and
-oracle in lock step for five rounds.  The draws come from a fixed seed, so
-every run checks the same cases.
+oracle in lock step for five rounds: even cases unit by unit
+(edit_outer_step_layer), odd cases as rounds (edit_outer_step_round, where
+units of up to 256 vectors are stepped whole in small launches).  The draws
+come from a fixed seed, so every run checks the same cases.
 """
 import numpy as np
 import pytest
@@ -55,7 +57,7 @@ def test_random_configuration(i):
                     std[j] *= 30.0
                 elif u < 0.2:
                     std[j] *= 1000.0
-            run.round(t, std=std, verbose=False)
+            run.round(t, std=std, verbose=False, via_round=i % 2 == 1)
     except NearTie as e:
         pytest.skip(str(e))
     finally:
