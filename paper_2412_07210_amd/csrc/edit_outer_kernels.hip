@@ -32,10 +32,13 @@
 // Pass 2, which writes as much as it reads, instead gives each thread one
 // vector and lets the block dispatcher order the traffic (see there).
 //
-// Also here: the Gram export/import of a sharded module (gram_reduce_kernel,
-// decide_gram_kernel), the one-pass mean step used when no penalty component
-// is on (fused_mean_kernel, fused_finish_kernel), and a plain copy kernel for
-// bandwidth and counter calibration.  Reductions go
+// Also here: the small launch of a round that steps units of one Gram-pass
+// block whole (round_small_kernel; the bodies of pass 1 and pass 2 are the
+// fragments gram_rows_valu.inc, gram_rows_mfma.inc and update_vector_at.inc,
+// shared with the kernels above), the Gram export/import of a sharded module
+// (gram_reduce_kernel, decide_gram_kernel), the one-pass mean step used when
+// no penalty component is on (fused_mean_kernel, fused_finish_kernel), and a
+// plain copy kernel for bandwidth and counter calibration.  Reductions go
 // wave shuffle -> LDS -> per-block partial -> one block in a fixed order, so
 // results are bitwise reproducible.
 #include "edit_outer_internal.h"
