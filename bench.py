@@ -18,6 +18,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -192,11 +193,21 @@ def _profile_cmds(variant: str) -> dict:
     }
 
 
-SHORT = {"pass1_gram_kernel": "pass1", "decide_kernel": "decide", "pass2_update_kernel": "pass2",
-         "fused_mean_kernel": "fused", "fused_finish_kernel": "finish"}
+# The two-unit Gram launch and the one-unit launch that takes two earlier
+# units' decisions are one kernel template (its last argument is the unit
+# count); they are told apart here.
+PAIR2, PAIR1 = "pass1_gram_pair_kernel<..., 2>", "pass1_gram_pair_kernel<..., 1>"
+PASS1_KINDS = ("pass1_gram_kernel", "pass1_gram_mfma_kernel", PAIR2, PAIR1)
+UNITS_PER_LAUNCH = {PAIR2: 2}
+
+SHORT = {"pass1_gram_kernel": "pass1", PAIR2: "pass1_pair", PAIR1: "pass1_pair1", "decide_kernel": "decide",
+         "pass2_update_kernel": "pass2", "fused_mean_kernel": "fused", "fused_finish_kernel": "finish"}
 
 
 def _kernel_kind(name: str) -> str:
+    m = re.search(r"pass1_gram_pair_kernel<[^>]*, (\d+)>", name)
+    if m:
+        return PAIR2 if m.group(1) == "2" else PAIR1
     for kind in ("pass1_gram_kernel", "pass1_gram_mfma_kernel", "decide_kernel", "pass2_update_kernel",
                  "round_small_kernel", "fused_mean_kernel", "fused_finish_kernel", "copy_kernel"):
         if kind in name:
@@ -237,12 +248,16 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
             if kind == "pass2_update_kernel" and -(-nvec // 128) * 128 == grid:
                 return n
             tpb = 768 if kind == "pass1_gram_mfma_kernel" else 256  # threads per Gram-pass block
-            if kind.startswith("pass1_gram") and -(-nvec // 256) >= grid // tpb - 1:
+            if kind in PASS1_KINDS and -(-nvec // 256) >= grid // tpb - 1:
                 return n
         return None
 
-    algo = lambda kind, n: {"pass1_gram_kernel": n * (4 + K * R), "pass1_gram_mfma_kernel": n * (4 + K * R),
-                            "pass2_update_kernel": n * (16 + 2 * K * R)}.get(kind)
+    # a two-unit launch counts two units of the size its grid matches (the
+    # workloads that pair units have units of one size)
+    def algo(kind, n):
+        if kind in PASS1_KINDS:
+            return UNITS_PER_LAUNCH.get(kind, 1) * n * (4 + K * R)
+        return n * (16 + 2 * K * R) if kind == "pass2_update_kernel" else None
     lines = [f"# Kernel durations by unit size: {wl.description}", "",
              "Command (from the repository root; `<out>` = the directory the profiler wrote to):", "",
              f"    rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace_{tag} -o {tag} -- "
@@ -262,8 +277,8 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
     # idle time between consecutive dispatches that are both steps of the
     # method (the stream's dependency latency; torch and copy kernels excluded)
     spans.sort()
-    ours = {"pass1_gram_kernel", "pass1_gram_mfma_kernel", "decide_kernel", "pass2_update_kernel",
-            "round_small_kernel", "fused_mean_kernel", "fused_finish_kernel"}
+    ours = {*PASS1_KINDS, "decide_kernel", "pass2_update_kernel", "round_small_kernel", "fused_mean_kernel",
+            "fused_finish_kernel"}
     pairs = [(a[2], b[2], b[0] - a[1]) for a, b in zip(spans, spans[1:]) if a[2] in ours and b[2] in ours]
     gaps = sorted(g for _, _, g in pairs)
     if gaps:
@@ -298,11 +313,11 @@ def summarize_profiles(out_dir: str, bench_json: str, variant: str = "two-pass")
     tag, sfx = cmds["tag"], cmds["suffix"]
     one = variant == "one-pass"
     kinds = ("fused_mean_kernel", "fused_finish_kernel") if one else \
-        ("pass1_gram_kernel", "decide_kernel", "pass2_update_kernel")
+        ("pass1_gram_kernel", PAIR2, PAIR1, "decide_kernel", "pass2_update_kernel")
     dominant = "fused_mean_kernel" if one else "pass2_update_kernel"
     wl = synth.get(DEFAULT_WORKLOAD)
     n, K, R = wl.layer_numel[0], wl.num_workers, wl.replica_bytes
-    algo = {"pass1_gram_kernel": n * (4 + K * R),
+    algo = {"pass1_gram_kernel": n * (4 + K * R), PAIR2: 2 * n * (4 + K * R), PAIR1: n * (4 + K * R),
             "pass2_update_kernel": n * (8 + K * R + 8 + K * R),
             "fused_mean_kernel": n * (8 + K * R + 8 + K * R)}
     title = "one-pass mean step (no penalty components)" if one else "outer step"

@@ -135,12 +135,14 @@ edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float *theta,
  * order on `stream` (the layer-wise synchronization of Sec. 3.1), with the
  * same results bit for bit as calling edit_outer_step_layer for each of them
  * in that order.  Up to K = 8 each unit's one-block decision runs inside
- * the next unit's pass-1 launch (an extra block), and its update pass
- * follows that launch; above K = 8 a unit's update pass follows its own
- * pass 1 and decision.  A unit of at most 256 16-byte vectors (2,048 bf16
- * or 1,024 fp32 elements) is stepped whole by one block of a small launch
- * that carries up to four such units, unless kernel timing
- * (edit_outer_set_profiling) covers it.
+ * the next pass-1 launch (an extra block), and its update pass follows that
+ * launch; two consecutive units (not the round's last) share one pass-1
+ * launch, whose partial sums are those of their own launches.  Above K = 8
+ * a unit's update pass follows its own pass 1 and decision.  A unit of at
+ * most 256 16-byte vectors (2,048 bf16 or 1,024 fp32 elements) is stepped
+ * whole by one block of a small launch that carries up to four such units.
+ * Units that kernel timing (edit_outer_set_profiling) covers keep launches
+ * of their own.
  *   layers   [count] unit indices, each at most once (else EDIT_EINVAL)
  *   theta    [count] device pointers, as in edit_outer_step_layer
  *   momentum [count] device pointers

@@ -61,6 +61,22 @@ struct SingleBlockDesc {
   int64_t n;
 };
 
+// A unit whose decision block 0 of a launch takes (see launch_pass1_pair).
+struct DecideDesc {
+  const double* partials;
+  int rows;
+  UnitRecord* rec;
+};
+
+// One unit of a two-unit Gram launch.
+struct Pass1Desc {
+  const float* theta;
+  const void* const* reps;  // host array of K device pointers (read at launch)
+  int64_t n;
+  double* partials;
+  int rows;
+};
+
 // Launchers (kernels.hip).  All enqueue on `stream` and return the launch
 // status; none synchronises.
 // Pass 1 over `rows` partial rows; when prev_partials is not null, one more
@@ -70,11 +86,16 @@ hipError_t launch_pass1(int K, bool bf16, int rows, const float* theta,
                         const void* const* reps, int64_t n, double* partials,
                         const double* prev_partials, int prev_rows, UnitRecord* prev_rec,
                         const DecideParams& prm, hipStream_t stream);
-// A small launch of a round: the decision of a previous unit (when
-// prev_partials is not null) and `count` whole single-block units.
-hipError_t launch_round_small(int K, bool bf16, const double* prev_partials, int prev_rows,
-                              UnitRecord* prev_rec, const DecideParams& prm, const SingleBlockDesc* unit,
-                              int count, double lr, double rho, hipStream_t stream);
+// Pass 1 of `count` (1 or 2) units of a round in one launch, K <= 8 only:
+// each block writes its row of every unit (the rows of its own launch), and
+// block 0 takes the decisions of `nprev` (0 to 2) earlier units first.
+hipError_t launch_pass1_pair(int K, bool bf16, const Pass1Desc* unit, int count, const DecideDesc* prev,
+                             int nprev, const DecideParams& prm, hipStream_t stream);
+// A small launch of a round: the decisions of `nprev` (0 to 2) earlier
+// units and `count` whole single-block units.
+hipError_t launch_round_small(int K, bool bf16, const DecideDesc* prev, int nprev, const DecideParams& prm,
+                              const SingleBlockDesc* unit, int count, double lr, double rho,
+                              hipStream_t stream);
 hipError_t launch_decide(int K, const double* partials, int rows, UnitRecord* rec,
                          const DecideParams& prm, hipStream_t stream);
 // The fixed-order sum of the partials as a K(K+1)/2 vector in device memory.

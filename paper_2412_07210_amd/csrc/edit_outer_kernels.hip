@@ -32,16 +32,20 @@
 // Pass 2, which writes as much as it reads, instead gives each thread one
 // vector and lets the block dispatcher order the traffic (see there).
 //
-// Also here: the small launch of a round that steps units of one Gram-pass
-// block whole (round_small_kernel; the bodies of pass 1 and pass 2 are the
-// fragments gram_rows_valu.inc, gram_rows_mfma.inc and update_vector_at.inc,
-// shared with the kernels above), the Gram export/import of a sharded module
+// Also here: the Gram pass of two units of a round in one launch
+// (pass1_gram_pair_kernel), the small launch of a round that steps units of
+// one Gram-pass block whole (round_small_kernel; the bodies of pass 1 and
+// pass 2 are the fragments gram_rows_valu.inc, gram_rows_mfma.inc and
+// update_vector_at.inc, shared with the kernels above), the Gram
+// export/import of a sharded module
 // (gram_reduce_kernel, decide_gram_kernel), the one-pass mean step used when
 // no penalty component is on (fused_mean_kernel, fused_finish_kernel), and a
 // plain copy kernel for bandwidth and counter calibration.  Reductions go
 // wave shuffle -> LDS -> per-block partial -> one block in a fixed order, so
 // results are bitwise reproducible.
 #include "edit_outer_internal.h"
+
+#include <algorithm>
 
 namespace edit {
 namespace {
@@ -401,6 +405,67 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_kernel(const fl
 #include "gram_rows_valu.inc"
 }
 
+// The decisions of up to two earlier units of a round (prev1 only with
+// prev0), one after the other in the calling block.
+template <int K>
+__device__ void run_prev_decisions(const PrevDecide& prev0, const PrevDecide& prev1,
+                                   const DecideParams& prm) {
+  run_prev_decide<K, pass1_threads<K>()>(prev0, prm);
+  if (prev1.partials) {
+    __syncthreads();  // the first decision has read the shared Gram
+    run_prev_decide<K, pass1_threads<K>()>(prev1, prm);
+  }
+}
+
+// One unit of a two-unit Gram launch (rows == 0: none).
+template <int K>
+struct Pass1Part {
+  const float* theta;
+  ConstPtrs<K> reps;
+  int64_t nvec;
+  int64_t n;
+  double* partials;
+  int rows;
+};
+
+// Pass 1 of two consecutive units of a round in one launch (K <= 8).  Each
+// block writes its partial row of the first unit, then the same row of the
+// second, so each unit gets exactly the partials of its own launch (same
+// rows, same order).  The persistent grid then starts and drains once for
+// the two units instead of twice; that start and drain costs about 13 us
+// per launch whatever the unit size.  Block 0 may take the decisions of the
+// two units before them.  UNITS = 1 is the launch of one unit that takes
+// two such decisions.
+template <int K, bool BF16, bool NT, int UNITS>
+__global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_pair_kernel(Pass1Part<K> unit0,
+                                                                   Pass1Part<K> unit1,
+                                                                   PrevDecide prev0,
+                                                                   PrevDecide prev1,
+                                                                   DecideParams prm) {
+  constexpr int NP = K * (K + 1) / 2;
+  constexpr int VE = Vec<BF16>::VE;
+  const int first = prev0.partials ? 1 : 0;
+  if (first && blockIdx.x == 0) {
+    run_prev_decisions<K>(prev0, prev1, prm);
+    return;
+  }
+  const int b = static_cast<int>(blockIdx.x) - first;  // this block's partial row of each unit
+#pragma unroll 1
+  for (int w = 0; w < UNITS; ++w) {
+    const int rows = w == 0 ? unit0.rows : unit1.rows;
+    if (b >= rows) continue;
+    if (w == 1) __syncthreads();  // the first unit's block reduction has read red[]
+    const float* __restrict__ theta = w == 0 ? unit0.theta : unit1.theta;
+    ConstPtrs<K> reps;
+#pragma unroll
+    for (int j = 0; j < K; ++j) reps.p[j] = w == 0 ? unit0.reps.p[j] : unit1.reps.p[j];
+    const int64_t nvec = w == 0 ? unit0.nvec : unit1.nvec;
+    const int64_t n = w == 0 ? unit0.n : unit1.n;
+    double* __restrict__ partials = w == 0 ? unit0.partials : unit1.partials;
+#include "gram_rows_valu.inc"
+  }
+}
+
 // Pass 1 for 8 < K <= 16: the Gram matrix sum_i d_i d_i^T over the unit's
 // elements is a rank-n update, and with K(K+1)/2 = 136 fp64 sums per lane a
 // VALU version runs out of registers.  It runs on the fp64 matrix cores as
@@ -720,15 +785,17 @@ __device__ void single_block_unit(const SingleBlockUnit<K>& su, const DecidePara
   }
 }
 
-// Block 0 takes the previous unit's decision when prev.partials is set; one
-// block per single-block unit steps that unit.  The blocks have the pass-1
-// kernel's size, so a unit's Gram row is the one its own pass 1 would write.
+// Block 0 takes the decisions of up to two earlier units when prev0.partials
+// is set; one block per single-block unit steps that unit.  The blocks have
+// the pass-1 kernel's size, so a unit's Gram row is the one its own pass 1
+// would write.
 template <int K, bool BF16, bool NT1, bool NT2, bool MFMA>
-__global__ __launch_bounds__(pass1_threads<K>()) void round_small_kernel(PrevDecide prev, DecideParams prm,
+__global__ __launch_bounds__(pass1_threads<K>()) void round_small_kernel(PrevDecide prev0, PrevDecide prev1,
+                                                               DecideParams prm,
                                                                SingleBlockUnits<K> single) {
-  const int first = prev.partials ? 1 : 0;
+  const int first = prev0.partials ? 1 : 0;
   if (first && blockIdx.x == 0) {
-    run_prev_decide<K, pass1_threads<K>()>(prev, prm);
+    run_prev_decisions<K>(prev0, prev1, prm);
     return;
   }
   const int sb = static_cast<int>(blockIdx.x) - first;
@@ -955,11 +1022,53 @@ hipError_t pass1_launch(int rows, const float* theta, const void* const* reps, i
   return hipGetLastError();
 }
 
+// Block 0's decisions: prev[0..nprev), nprev <= 2.
+inline void prev_decisions(const DecideDesc* prev, int nprev, PrevDecide& p0, PrevDecide& p1) {
+  p0 = nprev > 0 ? PrevDecide{prev[0].partials, prev[0].rows, prev[0].rec} : PrevDecide{nullptr, 0, nullptr};
+  p1 = nprev > 1 ? PrevDecide{prev[1].partials, prev[1].rows, prev[1].rec} : PrevDecide{nullptr, 0, nullptr};
+}
+
 template <int K, bool BF16>
-hipError_t round_small_launch(const double* prev_partials, int prev_rows, UnitRecord* prev_rec,
-                              const DecideParams& prm, const SingleBlockDesc* unit, int count, double lr,
-                              double rho, hipStream_t stream) {
-  const PrevDecide prev{prev_partials, prev_rows, prev_rec};
+Pass1Part<K> pass1_part(const Pass1Desc* unit, int count, int i) {
+  Pass1Part<K> part{};
+  if (i >= count) return part;  // rows 0: no unit
+  const Pass1Desc& d = unit[i];
+  part.theta = d.theta;
+  for (int j = 0; j < K; ++j) part.reps.p[j] = d.n > 0 ? d.reps[j] : nullptr;
+  part.nvec = d.n / Vec<BF16>::VE;
+  part.n = d.n;
+  part.partials = d.partials;
+  part.rows = d.rows;
+  return part;
+}
+
+template <int K, bool BF16>
+hipError_t pass1_pair_launch(const Pass1Desc* unit, int count, const DecideDesc* prev, int nprev,
+                             const DecideParams& prm, hipStream_t stream) {
+  if constexpr (K > 8) {
+    return hipErrorInvalidValue;  // the matrix-core Gram pass runs one unit per launch
+  } else {
+    PrevDecide p0, p1;
+    prev_decisions(prev, nprev, p0, p1);
+    const Pass1Part<K> u0 = pass1_part<K, BF16>(unit, count, 0);
+    const Pass1Part<K> u1 = pass1_part<K, BF16>(unit, count, 1);
+    const int blocks = (nprev > 0 ? 1 : 0) + std::max(u0.rows, u1.rows);
+    if (count == 2)
+      hipLaunchKernelGGL((pass1_gram_pair_kernel<K, BF16, kNT1, 2>), dim3(blocks), dim3(pass1_threads<K>()),
+                         0, stream, u0, u1, p0, p1, prm);
+    else
+      hipLaunchKernelGGL((pass1_gram_pair_kernel<K, BF16, kNT1, 1>), dim3(blocks), dim3(pass1_threads<K>()),
+                         0, stream, u0, u1, p0, p1, prm);
+    return hipGetLastError();
+  }
+}
+
+template <int K, bool BF16>
+hipError_t round_small_launch(const DecideDesc* prev, int nprev, const DecideParams& prm,
+                              const SingleBlockDesc* unit, int count, double lr, double rho,
+                              hipStream_t stream) {
+  PrevDecide p0, p1;
+  prev_decisions(prev, nprev, p0, p1);
   SingleBlockUnits<K> single{};
   single.count = count;
   single.lr = lr;
@@ -973,11 +1082,11 @@ hipError_t round_small_launch(const double* prev_partials, int prev_rows, UnitRe
     single.u[i].rec = d.rec;
     single.u[i].n = d.n;
   }
-  const int blocks = (prev_partials ? 1 : 0) + count;
+  const int blocks = (nprev > 0 ? 1 : 0) + count;
   if (blocks == 0) return hipSuccess;
   constexpr bool kMfma = K > 8;
   hipLaunchKernelGGL((round_small_kernel<K, BF16, kMfma ? kNTMfma : kNT1, kNT2, kMfma>), dim3(blocks),
-                     dim3(pass1_threads<K>()), 0, stream, prev, prm, single);
+                     dim3(pass1_threads<K>()), 0, stream, p0, p1, prm, single);
   return hipGetLastError();
 }
 
@@ -1069,17 +1178,30 @@ hipError_t launch_pass1(int K, bool bf16, int rows, const float* theta, const vo
   }
 }
 
-hipError_t launch_round_small(int K, bool bf16, const double* prev_partials, int prev_rows,
-                              UnitRecord* prev_rec, const DecideParams& prm, const SingleBlockDesc* unit,
-                              int count, double lr, double rho, hipStream_t stream) {
-  if (count < 0 || count > kMaxSingleBlockUnits) return hipErrorInvalidValue;
+hipError_t launch_pass1_pair(int K, bool bf16, const Pass1Desc* unit, int count, const DecideDesc* prev,
+                             int nprev, const DecideParams& prm, hipStream_t stream) {
+  if (count < 1 || count > 2 || nprev < 0 || nprev > 2) return hipErrorInvalidValue;
   switch (K) {
 #define EDIT_CASE(KK)                                                                              \
   case KK:                                                                                         \
-    return bf16 ? round_small_launch<KK, true>(prev_partials, prev_rows, prev_rec, prm, unit, count, \
-                                               lr, rho, stream)                                    \
-                : round_small_launch<KK, false>(prev_partials, prev_rows, prev_rec, prm, unit,     \
-                                                count, lr, rho, stream);
+    return bf16 ? pass1_pair_launch<KK, true>(unit, count, prev, nprev, prm, stream)               \
+                : pass1_pair_launch<KK, false>(unit, count, prev, nprev, prm, stream);
+    EDIT_FOR_EACH_K(EDIT_CASE)
+#undef EDIT_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_round_small(int K, bool bf16, const DecideDesc* prev, int nprev, const DecideParams& prm,
+                              const SingleBlockDesc* unit, int count, double lr, double rho,
+                              hipStream_t stream) {
+  if (count < 0 || count > kMaxSingleBlockUnits || nprev < 0 || nprev > 2) return hipErrorInvalidValue;
+  switch (K) {
+#define EDIT_CASE(KK)                                                                              \
+  case KK:                                                                                         \
+    return bf16 ? round_small_launch<KK, true>(prev, nprev, prm, unit, count, lr, rho, stream)     \
+                : round_small_launch<KK, false>(prev, nprev, prm, unit, count, lr, rho, stream);
     EDIT_FOR_EACH_K(EDIT_CASE)
 #undef EDIT_CASE
     default:

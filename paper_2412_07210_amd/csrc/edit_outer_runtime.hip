@@ -402,13 +402,35 @@ struct Enqueue {
                                 prev ? prev->rec : nullptr, prm, s);
     return e == hipSuccess ? EDIT_OK : fail_hip(e, "pass1 launch");
   }
-  // a small launch: the decision of `prev` (may be null) and whole
+  // pass 1 of one or two units (K <= 8) in one launch, whose block 0 takes
+  // the decisions of `nprev` earlier units first
+  edit_status_t pass1_pair(const int32_t* layer, float* const* theta, void* const* const* replicas,
+                           int count, const int32_t* prev, int nprev) {
+    Pass1Desc unit[2];
+    for (int i = 0; i < count; ++i) {
+      const Unit& u = h->units[layer[i]];
+      unit[i] = {theta[i], u.n == 0 ? kNoReplicas : const_cast<const void* const*>(replicas[i]), u.n,
+                 u.partials, u.rows};
+    }
+    DecideDesc dd[2];
+    describe(prev, nprev, dd);
+    hipError_t e = launch_pass1_pair(K, bf16, unit, count, dd, nprev, prm, s);
+    return e == hipSuccess ? EDIT_OK : fail_hip(e, "pass1 launch");
+  }
+  // a small launch: the decisions of `nprev` earlier units and whole
   // single-block units
-  edit_status_t small(Unit* prev, const SingleBlockDesc* single, int nsingle) {
-    hipError_t e = launch_round_small(K, bf16, prev ? prev->partials : nullptr, prev ? prev->rows : 0,
-                                      prev ? prev->rec : nullptr, prm, single, nsingle,
-                                      h->cfg.outer_lr, h->cfg.momentum, s);
+  edit_status_t small(const int32_t* prev, int nprev, const SingleBlockDesc* single, int nsingle) {
+    DecideDesc dd[2];
+    describe(prev, nprev, dd);
+    hipError_t e = launch_round_small(K, bf16, dd, nprev, prm, single, nsingle, h->cfg.outer_lr,
+                                      h->cfg.momentum, s);
     return e == hipSuccess ? EDIT_OK : fail_hip(e, "small launch");
+  }
+  void describe(const int32_t* layer, int count, DecideDesc* dd) const {
+    for (int i = 0; i < count; ++i) {
+      const Unit& u = h->units[layer[i]];
+      dd[i] = {u.partials, u.rows, u.rec};
+    }
   }
   edit_status_t gram_out(int32_t layer, double* gram) {
     Unit& u = h->units[layer];
@@ -601,66 +623,93 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
   // (one extra block, which would otherwise idle), and its pass 2 follows
   // that launch; the one-block decision then never holds up the whole chip
   // (measured at the 1B shape, same box: 14.63-14.68 ms per round against
-  // 14.79 ms with a decision kernel between each unit's two passes).  Above
-  // K = 8 the Gram pass is bound by fp64 arithmetic and reads through the
-  // cache, so a unit's pass 2 instead follows its own pass 1 with only the
-  // decision between them and finds the end of its input in the Infinity
-  // Cache (measured at K = 16: 696 against 730 us per 51.4M-element pass 2).
+  // 14.79 ms with a decision kernel between each unit's two passes).  Two
+  // consecutive units also share one pass-1 launch (not the round's last
+  // unit, whose decision would then wait for the other's), so the persistent
+  // grid starts and drains once per pair; the next launch then takes both
+  // decisions.  Above K = 8 the Gram pass is bound by fp64 arithmetic and
+  // reads through the cache, so a unit's pass 2 instead follows its own pass
+  // 1 with only the decision between them and finds the end of its input in
+  // the Infinity Cache (measured at K = 16: 696 against 730 us per
+  // 51.4M-element pass 2).
   //
   // A unit whose Gram pass is one block is stepped whole by one block of a
   // small launch, up to kMaxSingleBlockUnits per launch (its own two
   // launches cost about 16 us at K = 16, its work a few microseconds); a
-  // small launch also carries the pending decision.  Such units are
+  // small launch also carries the pending decisions.  Such units are
   // independent of the others, so this only changes which launch runs them.
   // Units whose kernels are being timed keep their own launches.
   const bool adjacent = K > 8;
-  int32_t pending = -1;  // index i of the unit whose decision is not launched yet
+  int32_t pend[2];  // indices i of the units whose decisions are not launched yet
+  int32_t pend_layer[2];
+  int npend = 0;
   SingleBlockDesc single[kMaxSingleBlockUnits];
   int nsingle = 0;
-  auto flush_pass2 = [&](int32_t i) -> edit_status_t {
-    const int32_t l = layers[i];
-    void* const* reps = replicas + static_cast<size_t>(i) * K;
-    EDIT_TRY(q.event(h->units[l], l, 2));
-    EDIT_TRY(q.pass2(l, theta[i], momentum[i], reps));
-    return q.event(h->units[l], l, 3);
-  };
-  // the pending decision (if any) and the waiting single-block units, then
-  // the pending unit's pass 2
-  auto flush_small = [&]() -> edit_status_t {
-    EDIT_TRY(q.small(pending >= 0 ? &h->units[layers[pending]] : nullptr, single, nsingle));
-    nsingle = 0;
-    if (pending >= 0) EDIT_TRY(flush_pass2(pending));
-    pending = -1;
+  auto reps_of = [&](int32_t i) { return replicas + static_cast<size_t>(i) * K; };
+  auto rider = [&](int32_t i) { return h->units[layers[i]].rows == 1 && !q.profiled(layers[i]); };
+  // pass 2 of the pending units, whose decisions the last launch took
+  auto flush_pass2 = [&]() -> edit_status_t {
+    for (int k = 0; k < npend; ++k) {
+      const int32_t i = pend[k], l = layers[i];
+      EDIT_TRY(q.event(h->units[l], l, 2));
+      EDIT_TRY(q.pass2(l, theta[i], momentum[i], reps_of(i)));
+      EDIT_TRY(q.event(h->units[l], l, 3));
+    }
+    npend = 0;
     return EDIT_OK;
+  };
+  // the pending decisions and the waiting single-block units, then the
+  // pending units' pass 2
+  auto flush_small = [&]() -> edit_status_t {
+    EDIT_TRY(q.small(pend_layer, npend, single, nsingle));
+    nsingle = 0;
+    return flush_pass2();
   };
   for (int32_t i = 0; i < count; ++i) {
     const int32_t l = layers[i];
     Unit& u = h->units[l];
-    if (u.rows == 1 && !q.profiled(l)) {
-      single[nsingle++] = {theta[i], momentum[i], replicas + static_cast<size_t>(i) * K, u.partials,
-                           u.rec, u.n};
+    if (rider(i)) {
+      single[nsingle++] = {theta[i], momentum[i], reps_of(i), u.partials, u.rec, u.n};
       if (nsingle == kMaxSingleBlockUnits) EDIT_TRY(flush_small());
       continue;
     }
     if (nsingle > 0) {
       EDIT_TRY(flush_small());
-    } else if (adjacent && pending >= 0) {
-      EDIT_TRY(q.decide(layers[pending]));
-      EDIT_TRY(flush_pass2(pending));
-      pending = -1;
+    } else if (adjacent && npend > 0) {
+      EDIT_TRY(q.decide(pend_layer[0]));
+      EDIT_TRY(flush_pass2());
     }
-    Unit* prev = pending >= 0 ? &h->units[layers[pending]] : nullptr;
+    const bool pair = !adjacent && !q.profiled(l) && i + 2 < count && !rider(i + 1) &&
+                      !q.profiled(layers[i + 1]);
+    if (pair) {
+      float* const th2[2] = {theta[i], theta[i + 1]};
+      void* const* const rp2[2] = {reps_of(i), reps_of(i + 1)};
+      EDIT_TRY(q.pass1_pair(layers + i, th2, rp2, 2, pend_layer, npend));
+      EDIT_TRY(flush_pass2());
+      pend[0] = i, pend_layer[0] = l;
+      pend[1] = i + 1, pend_layer[1] = layers[i + 1];
+      npend = 2;
+      ++i;
+      continue;
+    }
     EDIT_TRY(q.event(u, l, 0));
-    EDIT_TRY(q.pass1(l, theta[i], replicas + static_cast<size_t>(i) * K, prev));
+    if (npend == 2) {  // both decisions of the pair before it
+      float* const th1[1] = {theta[i]};
+      void* const* const rp1[1] = {reps_of(i)};
+      EDIT_TRY(q.pass1_pair(layers + i, th1, rp1, 1, pend_layer, npend));
+    } else {
+      EDIT_TRY(q.pass1(l, theta[i], reps_of(i), npend ? &h->units[pend_layer[0]] : nullptr));
+    }
     EDIT_TRY(q.event(u, l, 1));
-    if (pending >= 0) EDIT_TRY(flush_pass2(pending));
-    pending = i;
+    EDIT_TRY(flush_pass2());
+    pend[0] = i, pend_layer[0] = l;
+    npend = 1;
   }
-  if (nsingle > 0) {
+  if (nsingle > 0 || npend == 2) {
     EDIT_TRY(flush_small());
-  } else if (pending >= 0) {
-    EDIT_TRY(q.decide(layers[pending]));
-    EDIT_TRY(flush_pass2(pending));
+  } else if (npend == 1) {
+    EDIT_TRY(q.decide(pend_layer[0]));
+    EDIT_TRY(flush_pass2());
   }
   return q.finish_round(layers, count);
 }
