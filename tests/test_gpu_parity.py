@@ -371,6 +371,71 @@ def test_single_block_units_in_a_round_match_unit_by_unit(K, dtype):
         assert x.round == y.round == 3
 
 
+# Round schedules around the shared Gram launch (K <= 8): B = a unit of more
+# than one Gram-pass block, S = a single-block unit.  (name, sizes, timing)
+_PAIR_SCHEDULES = [
+    # B B B B B: two pairs, the round's last unit alone
+    ("pairs", [300_001, 65_537, 1_000_003, 40_000, 123_457], 0),
+    # B B S B B B S S B: riders after a pair carry both of its decisions
+    ("pairs_riders", [300_001, 65_537, 2_048, 100_000, 77_777, 50_000, 1_000, 5, 150_001], 0),
+    # B B S: the round ends on a rider that carries a pair's decisions
+    ("pair_rider_end", [300_001, 65_537, 33], 0),
+    # eight B with every third unit timed: timed units run alone, one after a
+    # pair takes both of its decisions
+    ("timed", [200_003, 65_537, 90_000, 120_001, 40_000, 77_777, 100_000, 50_001], 3),
+]
+
+
+@pytest.mark.parametrize("K,dtype", [(8, "bf16"), (5, "f32")])
+@pytest.mark.parametrize("name,sizes,every", _PAIR_SCHEDULES, ids=[s[0] for s in _PAIR_SCHEDULES])
+def test_shared_gram_launches_match_unit_by_unit(K, dtype, name, sizes, every):
+    """Rounds whose consecutive units share a Gram-pass launch, in every
+    schedule the round path builds around it, give the bits of unit-by-unit
+    edit_outer_step_layer calls over three rounds (the second with one worker
+    x1000, so the decisions differ between units).  Timed units report
+    positive kernel times."""
+    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=1,
+                     name=f"pairs{name}{K}{dtype}")
+    print(f"schedule {name}: K={K} {dtype} sizes={sizes} timing every {every}", flush=True)
+    results = []
+    for mode in ("layer", "round"):
+        h = EditOuter(OuterConfig(K, wl.layer_numel, dtype, ema_warmup_rounds=1), DEV)
+        h.set_profiling(every)
+        units = [_fresh_inputs(wl, u, 0, DEV) for u in range(wl.num_units)]
+        for t in range(3):
+            std = wl.worker_std(t)
+            if t == 1:
+                std[K - 1] *= 1000.0
+            for u in range(wl.num_units):
+                wl.fill_replicas(units[u][0], units[u][2], u, t, std=std)
+            torch.cuda.synchronize()
+            if mode == "layer":
+                for u in range(wl.num_units):
+                    h.step_layer(u, *units[u])
+            else:
+                h.step_round(units)
+            torch.cuda.synchronize()
+            if t == 1:
+                flagged = [h.state_get(u) for u in range(wl.num_units)]
+        results.append((units, flagged + [h.state_get(u) for u in range(wl.num_units)]))
+        if mode == "round" and every:
+            for u in range(0, wl.num_units, every):
+                p1, p2 = h.kernel_times(u)
+                assert p1 > 0 and p2 > 0, f"unit {u}: kernel times {p1}, {p2}"
+        h.close()
+    (ua, sa), (ub, sb) = results
+    for u, (a, b) in enumerate(zip(ua, ub)):
+        assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1]), f"unit {u}"
+        assert all(torch.equal(x, y) for x, y in zip(a[2], b[2])), f"unit {u}"
+    for x, y in zip(sa, sb):
+        for f in ("norm", "ema_mean", "ema_std", "weight", "anomalous"):
+            assert np.array_equal(getattr(x, f), getattr(y, f)), f
+        assert x.synced_norm == y.synced_norm and x.clip_coef == y.clip_coef
+    n = wl.num_units
+    assert all(s.round == 2 for s in sb[:n]) and all(s.round == 3 for s in sb[n:])
+    assert all(s.anomalous[K - 1] for s in sb[:n]), "the x1000 worker was not flagged in every unit"
+
+
 def test_state_get_waits_for_its_round_through_the_event_ring():
     """A round's units share one completion event from a small ring.  Seven
     rounds are enqueued on two streams without any host synchronisation
