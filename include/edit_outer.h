@@ -293,12 +293,11 @@ void edit_group_destroy(edit_group_t h);
 edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t every);
 
 /* Durations in ms of the last profiled step of `layer`: ms[0] its norm/Gram
- * pass plus its decision kernel (in a round: its norm/Gram launch, which up
- * to K = 8 also carries the previous unit's decision), ms[1] its update
- * pass.  With
- * EDIT_ONE_PASS: ms[0] the fused pass, ms[1] the record reduction when the
- * unit was stepped alone (0 in a round, which reduces all units in one launch
- * at its end).  Waits for it. */
+ * pass plus its decision kernel (in a round: its own norm/Gram launch, which
+ * up to K = 8 also carries the decisions of the one or two units before it),
+ * ms[1] its update pass.  With EDIT_ONE_PASS: ms[0] the fused pass, ms[1]
+ * the record reduction when the unit was stepped alone (0 in a round, which
+ * reduces all units in one launch at its end).  Waits for it. */
 edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[2]);
 
 /* Plain device-to-device copy kernel of nbytes (a multiple of 16, 16-byte
