@@ -371,26 +371,32 @@ def test_single_block_units_in_a_round_match_unit_by_unit(K, dtype):
         assert x.round == y.round == 3
 
 
-# Round schedules around the shared Gram launch (K <= 8): B = a unit of more
-# than one Gram-pass block, S = a single-block unit.  (name, sizes, timing)
+# Round schedules around the shared Gram launch (K <= 8; two consecutive
+# units per launch): B = a unit of more than one Gram-pass block, S = a
+# single-block unit.  (name, sizes, timing)
 _PAIR_SCHEDULES = [
     # B B B B B: two pairs, the round's last unit alone
     ("pairs", [300_001, 65_537, 1_000_003, 40_000, 123_457], 0),
+    # eleven B: five pairs in a row, each launch taking the previous pair's decisions
+    ("pair_chain", [90_001, 65_537, 40_000, 70_007, 33_333, 100_000, 55_555, 81_920, 47_111, 60_000, 99_999], 0),
     # B B S B B B S S B: riders after a pair carry both of its decisions
     ("pairs_riders", [300_001, 65_537, 2_048, 100_000, 77_777, 50_000, 1_000, 5, 150_001], 0),
     # B B S: the round ends on a rider that carries a pair's decisions
     ("pair_rider_end", [300_001, 65_537, 33], 0),
-    # eight B with every third unit timed: timed units run alone, one after a
-    # pair takes both of its decisions
-    ("timed", [200_003, 65_537, 90_000, 120_001, 40_000, 77_777, 100_000, 50_001], 3),
+    # nine B with every fourth unit timed: a pair and a unit alone between
+    # timed units
+    ("timed4", [200_003, 65_537, 90_000, 120_001, 40_000, 77_777, 100_000, 50_001, 70_000], 4),
+    # eight B with every third unit timed: a timed unit after a pair takes
+    # both of its decisions
+    ("timed3", [200_003, 65_537, 90_000, 120_001, 40_000, 77_777, 100_000, 50_001], 3),
 ]
 
 
 @pytest.mark.parametrize("K,dtype", [(8, "bf16"), (5, "f32")])
 @pytest.mark.parametrize("name,sizes,every", _PAIR_SCHEDULES, ids=[s[0] for s in _PAIR_SCHEDULES])
 def test_shared_gram_launches_match_unit_by_unit(K, dtype, name, sizes, every):
-    """Rounds whose consecutive units share a Gram-pass launch, in every
-    schedule the round path builds around it, give the bits of unit-by-unit
+    """Rounds whose consecutive units share a Gram-pass launch, in the
+    schedules the round path builds around it, give the bits of unit-by-unit
     edit_outer_step_layer calls over three rounds (the second with one worker
     x1000, so the decisions differ between units).  Timed units report
     positive kernel times."""
