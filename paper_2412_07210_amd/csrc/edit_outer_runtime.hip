@@ -619,7 +619,7 @@ edit_status_t edit_outer_step_round(edit_outer_t h, int32_t count, const int32_t
     EDIT_TRY(q.records(0, h->cfg.num_layers));
     return q.finish_round(layers, count);
   }
-  // Up to K = 8 every unit's decision rides in the next unit's pass-1 launch
+  // Up to K = 8 every unit's decision rides in the next pass-1 launch
   // (one extra block, which would otherwise idle), and its pass 2 follows
   // that launch; the one-block decision then never holds up the whole chip
   // (measured at the 1B shape, same box: 14.63-14.68 ms per round against
