@@ -44,8 +44,11 @@
 extern "C" {
 #endif
 
-/* Largest number of workers per sync group the kernels are built for. */
-#define EDIT_MAX_K 16
+/* Largest number of workers per sync group (the K of Sec. 3.1's model sync
+ * group; the paper fixes no upper bound).  Kernels are specialised for every
+ * K in 1..EDIT_MAX_K: the Gram pass keeps the K(K+1)/2 pairwise sums in
+ * fp64 vector registers up to K = 8 and uses the fp64 matrix cores above. */
+#define EDIT_MAX_K 32
 
 /* Penalty components; clearing all three gives the DiLoCo outer step
  * (the ablations of Sec. 4.5). */
@@ -68,6 +71,7 @@ extern "C" {
 
 typedef struct edit_outer *edit_outer_t; /* opaque, library-owned */
 
+/* Status of every call; nothing is thrown across the ABI. */
 typedef enum {
   EDIT_OK = 0,
   EDIT_EINVAL = -1, /* bad argument: index, size, NULL, alignment, aliasing  */
@@ -77,8 +81,12 @@ typedef enum {
   EDIT_ENODEV = -5  /* the current device is not a gfx950 GPU                 */
 } edit_status_t;
 
+/* Element type of the K replicas (the paper states no precision; theta and
+ * the momentum are always fp32). */
 typedef enum { EDIT_F32 = 0, EDIT_BF16 = 1 } edit_dtype_t;
 
+/* Hyper-parameters of the outer step (Sec. 3.2 and the training settings of
+ * Sec. 4.1), the sync units and the replica type. */
 typedef struct {
   int32_t num_workers;        /* K, 1..EDIT_MAX_K                              */
   int32_t num_layers;         /* L sync units (modules), >= 1                  */
@@ -91,10 +99,16 @@ typedef struct {
   double clip_eps;            /* eps of Eq. 4, > 0                             */
   double ema_alpha;           /* alpha of Eq. 1 (paper: 0.02), in (0, 1]       */
   double z_threshold;         /* delta of the z-test (paper: 3)                */
-  int64_t ema_warmup_rounds;  /* rounds per unit with no anomaly flagging      */
+  int64_t ema_warmup_rounds;  /* rounds per unit with no anomaly flagging, at  */
+                              /* least edit_outer_min_warmup(alpha, delta)      */
+                              /* when EDIT_AE is set (see there)                */
 } edit_outer_config_t;
 
-/* Per-unit state and the decision of its most recent step (host memory). */
+/* Per-unit state and the decision of its most recent step (host memory):
+ * the EMA mean and std of each worker's pseudo-gradient norm (Eq. 1, kept
+ * per worker and module as Sec. 3.2 describes), the norms G_j, the anomaly
+ * mask, the weights w_j of Eq. 2, ||Delta_bar|| and the clip factor beta of
+ * Eq. 4. */
 typedef struct {
   int64_t round;               /* completed outer rounds of this unit         */
   int32_t num_workers;         /* K                                           */
@@ -110,11 +124,26 @@ typedef struct {
   double clip_coef;            /* beta of the last step (0 on rollback)       */
 } edit_layer_state_t;
 
-/* Create a handle on the current device.  Validates cfg (K range, L >= 1,
- * numel >= 0, dtype, 0 < alpha <= 1, eps > 0, non-negative warm-up),
- * allocates the EMA state (zero), per-unit scratch and events.
- * EDIT_EINVAL for a bad config, EDIT_ENODEV off gfx950, EDIT_ENOMEM. */
+/* Create a handle on the current device for L sync units, each holding the
+ * state Sec. 3.2 keeps per module: the EMA mean and std of Eq. 1 for each of
+ * the K workers, zero at the start (the paper gives no initial value), and a
+ * round counter.  Validates cfg (K in 1..EDIT_MAX_K, L >= 1, numel >= 0,
+ * dtype, 0 < alpha <= 1, eps > 0, and with EDIT_AE a warm-up of at least
+ * edit_outer_min_warmup rounds), allocates the state, per-unit scratch and
+ * events.  EDIT_EINVAL for a bad config, EDIT_ENODEV off gfx950,
+ * EDIT_ENOMEM. */
 edit_status_t edit_outer_init(const edit_outer_config_t *cfg, edit_outer_t *out);
+
+/* The shortest EMA warm-up, in rounds, after which a worker whose norm G_j
+ * is the same every round passes the z-test of Eq. 1 (G_j - mu_j > delta *
+ * sigma_j flags it) when the EMA starts from zero: mu after k updates is
+ * G (1 - (1-alpha)^k), so it lags G, and sigma is small.  With a shorter
+ * warm-up every such worker is flagged at its first tested round, and since
+ * a flagged worker's EMA state is not updated (Sec. 3.2), the unit stays
+ * masked or rolled back from then on.  6 for the paper's alpha = 0.02 and
+ * delta = 3.  -1 when no warm-up suffices (delta <= 0) or alpha is outside
+ * (0, 1].  Host-only; no device needed. */
+int64_t edit_outer_min_warmup(double alpha, double delta);
 
 /* One outer step of unit `layer` (Sec. 3.2, Algorithm 2), enqueued on
  * `stream` (a hipStream_t; NULL = the default stream).  No host
@@ -206,19 +235,25 @@ edit_status_t edit_outer_apply_layer(edit_outer_t h, int32_t layer, const double
                                      float *theta, float *momentum, void *const *replicas,
                                      void *stream);
 
-/* Copy unit `layer`'s EMA state and last decision to *out, after waiting for
- * that unit's last enqueued step.  EDIT_ESTATE if the unit never stepped and
- * no state was set. */
+/* Copy unit `layer`'s EMA state (Eq. 1: mu_j and sigma_j of every worker,
+ * the per-module state of Sec. 3.2) and last decision (G_j, mask, w_j of
+ * Eq. 2, ||Delta_bar||, beta of Eq. 4) to *out (host memory), after waiting
+ * for that unit's last enqueued step.  EDIT_ESTATE if the unit never stepped
+ * and no state was set. */
 edit_status_t edit_outer_state_get(edit_outer_t h, int32_t layer, edit_layer_state_t *out);
 
-/* Restore unit `layer`'s EMA state (ema_mean, ema_std, round; other fields
- * ignored), e.g. when resuming from a checkpoint.  Waits for that unit's
+/* Restore unit `layer`'s EMA state of Eq. 1 (ema_mean, ema_std and the
+ * round counter that the warm-up of Sec. 3.2 counts; other fields ignored),
+ * e.g. when resuming from a checkpoint.  EDIT_EINVAL for a non-finite mean,
+ * a negative or non-finite std or a negative round.  Waits for that unit's
  * last enqueued step first. */
 edit_status_t edit_outer_state_set(edit_outer_t h, int32_t layer, const edit_layer_state_t *in);
 
-/* Release everything the handle owns (waits for its pending work). */
+/* Release everything the handle owns: the per-unit state of Sec. 3.2, the
+ * scratch memory and the events (waits for its pending work first). */
 void edit_outer_destroy(edit_outer_t h);
 
+/* A static string naming status s. */
 const char *edit_outer_strerror(edit_status_t s);
 
 /* Message of the last failure on the calling thread ("" if none). */

@@ -6,5 +6,5 @@ synthetic workloads shaped like Llama decoder layers.
 """
 from .outer import (  # noqa: F401
     AE, GC, ONE_PASS, WA, EditOuter, EditOuterError, LayerState, OuterConfig, SyncGroupWorker,
-    copy_probe, load_library,
+    copy_probe, load_library, min_warmup,
 )

@@ -3,11 +3,13 @@
     python -m paper_2412_07210_amd.build
 
 Each source compiles to an object under paper_2412_07210_amd/_build/ (in
-parallel), then links into paper_2412_07210_amd/libedit_outer.so.
+parallel; the kernels file once per range of worker counts), then links into
+paper_2412_07210_amd/libedit_outer.so.
 """
 from __future__ import annotations
 
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -19,7 +21,10 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIBRARY = os.path.join(PKG, "libedit_outer.so")
-SOURCES = ["edit_outer_kernels.hip", "edit_outer_runtime.hip", "edit_group_kernels.hip", "edit_group_runtime.hip"]
+SOURCES = ["edit_outer_dispatch.hip", "edit_outer_runtime.hip", "edit_group_kernels.hip", "edit_group_runtime.hip"]
+# Compiled once per range of worker counts K (EDIT_K_RANGES in
+# edit_outer_internal.h), so its template instantiations build in parallel.
+KERNELS = "edit_outer_kernels.hip"
 ARCH = "gfx950"
 
 # -packed-fp32-ops off: no v_pk_* fp32 instructions are generated.
@@ -37,9 +42,25 @@ def hipcc() -> str:
     return path
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+def k_ranges() -> list:
+    """[(first K, last K)] of the per-range objects of the kernels file."""
+    text = open(os.path.join(CSRC, "edit_outer_internal.h")).read()
+    line = re.search(r"#define EDIT_K_RANGES\(X\)(.*)", text).group(1)
+    return [(int(a), int(b)) for a, b in re.findall(r"X\((\d+), (\d+)\)", line)]
+
+
+def _jobs() -> list:
+    """(source, object name, extra flags) of every compile."""
+    jobs = [(src, os.path.splitext(src)[0], []) for src in SOURCES]
+    for a, b in k_ranges():
+        jobs.append((KERNELS, f"edit_outer_kernels_k{a}_{b}", [f"-DEDIT_K_FIRST={a}", f"-DEDIT_K_LAST={b}"]))
+    return jobs
+
+
+def _compile(job, verbose: bool) -> str:
+    src, name, extra = job
+    obj = os.path.join(BUILD_DIR, name + ".o")
+    cmd = [hipcc(), *HIPCC_FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -56,8 +77,9 @@ def _compile(src: str, verbose: bool) -> str:
 def build(verbose: bool = False) -> str:
     """Compile every HIP source and link the shared library; return its path."""
     os.makedirs(BUILD_DIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as pool:
-        objs = list(pool.map(lambda s: _compile(s, verbose), SOURCES))
+    jobs = _jobs()
+    with ThreadPoolExecutor(max_workers=min(len(jobs), os.cpu_count() or 1)) as pool:
+        objs = list(pool.map(lambda j: _compile(j, verbose), jobs))
     tmp = LIBRARY + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     if verbose:

@@ -1,0 +1,88 @@
+// Launchers of the outer-step kernels by worker count K: each call finds the
+// kernel set of K's range (one object of edit_outer_kernels.hip per range)
+// and forwards to it.  Host code only.
+#include "edit_outer_internal.h"
+
+namespace edit {
+namespace {
+
+const KernelSet* kernels_for(int K) {
+#define EDIT_RANGE(first, last) \
+  if (K >= (first) && K <= (last)) return EDIT_KERNEL_SET_FN(first)(K);
+  EDIT_K_RANGES(EDIT_RANGE)
+#undef EDIT_RANGE
+  return nullptr;
+}
+
+}  // namespace
+
+hipError_t launch_pass1(int K, bool bf16, int rows, const float* theta, const void* const* reps,
+                        int64_t n, double* partials, const double* prev_partials, int prev_rows,
+                        UnitRecord* prev_rec, const DecideParams& prm, hipStream_t stream) {
+  const KernelSet* s = kernels_for(K);
+  return s ? s->pass1(bf16, rows, theta, reps, n, partials, prev_partials, prev_rows, prev_rec, prm, stream)
+           : hipErrorInvalidValue;
+}
+
+hipError_t launch_pass1_pair(int K, bool bf16, const Pass1Desc* unit, int count, const DecideDesc* prev,
+                             int nprev, const DecideParams& prm, hipStream_t stream) {
+  if (count < 1 || count > 2 || nprev < 0 || nprev > 2) return hipErrorInvalidValue;
+  const KernelSet* s = kernels_for(K);
+  return s ? s->pass1_pair(bf16, unit, count, prev, nprev, prm, stream) : hipErrorInvalidValue;
+}
+
+hipError_t launch_round_small(int K, bool bf16, const DecideDesc* prev, int nprev, const DecideParams& prm,
+                              const SingleBlockDesc* unit, int count, double lr, double rho,
+                              hipStream_t stream) {
+  if (count < 0 || count > kMaxSingleBlockUnits || nprev < 0 || nprev > 2) return hipErrorInvalidValue;
+  const KernelSet* s = kernels_for(K);
+  return s ? s->round_small(bf16, prev, nprev, prm, unit, count, lr, rho, stream) : hipErrorInvalidValue;
+}
+
+hipError_t launch_decide(int K, const double* partials, int rows, UnitRecord* rec, const DecideParams& prm,
+                         hipStream_t stream) {
+  const KernelSet* s = kernels_for(K);
+  return s ? s->decide(partials, rows, rec, prm, stream) : hipErrorInvalidValue;
+}
+
+hipError_t launch_gram_reduce(int K, const double* partials, int rows, double* gram, hipStream_t stream) {
+  const KernelSet* s = kernels_for(K);
+  return s ? s->gram_reduce(partials, rows, gram, stream) : hipErrorInvalidValue;
+}
+
+hipError_t launch_decide_gram(int K, const double* gram, UnitRecord* rec, const DecideParams& prm,
+                              hipStream_t stream) {
+  const KernelSet* s = kernels_for(K);
+  return s ? s->decide_gram(gram, rec, prm, stream) : hipErrorInvalidValue;
+}
+
+hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom, void* const* reps,
+                        const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
+  const KernelSet* s = kernels_for(K);
+  return s ? s->pass2(bf16, blocks, theta, mom, reps, rec, n, lr, rho, stream) : hipErrorInvalidValue;
+}
+
+int fused_vectors_per_thread(int K, bool bf16) {
+  const KernelSet* s = kernels_for(K);
+  return s ? (bf16 ? s->fused_vectors_bf16 : s->fused_vectors_f32) : 1;
+}
+
+hipError_t launch_fused_mean(int K, bool bf16, int rows, float* theta, float* mom, void* const* reps,
+                             double* partials, UnitRecord* rec, int64_t n, double lr, double rho,
+                             hipStream_t stream) {
+  const KernelSet* s = kernels_for(K);
+  return s ? s->fused_mean(bf16, rows, theta, mom, reps, partials, rec, n, lr, rho, stream)
+           : hipErrorInvalidValue;
+}
+
+hipError_t launch_fused_finish(int K, const FinishEntry* table, int units, hipStream_t stream) {
+  const KernelSet* s = kernels_for(K);
+  return s ? s->fused_finish(table, units, stream) : hipErrorInvalidValue;
+}
+
+int pass1_blocks_per_cu(int K, bool bf16) {
+  const KernelSet* s = kernels_for(K);
+  return s ? s->pass1_blocks_per_cu(bf16) : 1;
+}
+
+}  // namespace edit

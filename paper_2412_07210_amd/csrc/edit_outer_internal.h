@@ -77,8 +77,43 @@ struct Pass1Desc {
   int rows;
 };
 
-// Launchers (kernels.hip).  All enqueue on `stream` and return the launch
-// status; none synchronises.
+// The kernels specialised for one K, behind plain function pointers.  The
+// kernels file is compiled once per range of K below (the ranges' template
+// instantiations then compile in parallel); the object of the range that
+// starts at F exports EDIT_KERNEL_SET_FN(F)(K), which returns the set of a K
+// in its range and nullptr otherwise.
+#define EDIT_K_RANGES(X) X(1, 8) X(9, 16) X(17, 24) X(25, 32)
+#define EDIT_KERNEL_SET_FN2(first) kernel_set_from_##first
+#define EDIT_KERNEL_SET_FN(first) EDIT_KERNEL_SET_FN2(first)
+
+struct KernelSet {
+  hipError_t (*pass1)(bool bf16, int rows, const float* theta, const void* const* reps, int64_t n,
+                      double* partials, const double* prev_partials, int prev_rows, UnitRecord* prev_rec,
+                      const DecideParams& prm, hipStream_t stream);
+  hipError_t (*pass1_pair)(bool bf16, const Pass1Desc* unit, int count, const DecideDesc* prev, int nprev,
+                           const DecideParams& prm, hipStream_t stream);
+  hipError_t (*round_small)(bool bf16, const DecideDesc* prev, int nprev, const DecideParams& prm,
+                            const SingleBlockDesc* unit, int count, double lr, double rho, hipStream_t stream);
+  hipError_t (*decide)(const double* partials, int rows, UnitRecord* rec, const DecideParams& prm,
+                       hipStream_t stream);
+  hipError_t (*gram_reduce)(const double* partials, int rows, double* gram, hipStream_t stream);
+  hipError_t (*decide_gram)(const double* gram, UnitRecord* rec, const DecideParams& prm, hipStream_t stream);
+  hipError_t (*pass2)(bool bf16, int blocks, float* theta, float* mom, void* const* reps, const UnitRecord* rec,
+                      int64_t n, double lr, double rho, hipStream_t stream);
+  hipError_t (*fused_mean)(bool bf16, int rows, float* theta, float* mom, void* const* reps, double* partials,
+                           UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream);
+  hipError_t (*fused_finish)(const FinishEntry* table, int units, hipStream_t stream);
+  int (*pass1_blocks_per_cu)(bool bf16);
+  int fused_vectors_bf16, fused_vectors_f32;
+};
+
+#define EDIT_DECLARE_SET(first, last) const KernelSet* EDIT_KERNEL_SET_FN(first)(int K);
+EDIT_K_RANGES(EDIT_DECLARE_SET)
+#undef EDIT_DECLARE_SET
+
+// Launchers (edit_outer_dispatch.hip, through the kernel sets).  All enqueue
+// on `stream` and return the launch status (hipErrorInvalidValue for a K
+// outside 1..EDIT_MAX_K); none synchronises.
 // Pass 1 over `rows` partial rows; when prev_partials is not null, one more
 // block takes the decision of the previous unit of a round (prev_rows rows,
 // record prev_rec) inside the same launch.
@@ -108,10 +143,10 @@ hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom,
                         void* const* reps, const UnitRecord* rec, int64_t n, double lr,
                         double rho, hipStream_t stream);
 // One-pass mean step (no penalty components): `rows` blocks of
-// fused_vectors_per_thread(bf16) * kFusedThreads vectors each, leaving
+// fused_vectors_per_thread(K, bf16) * kFusedThreads vectors each, leaving
 // (K+1) x rows norm partials and the unit marked; then one block per entry
 // of `table` turns marked units' partials into their records.
-int fused_vectors_per_thread(bool bf16);
+int fused_vectors_per_thread(int K, bool bf16);
 hipError_t launch_fused_mean(int K, bool bf16, int rows, float* theta, float* mom,
                              void* const* reps, double* partials, UnitRecord* rec, int64_t n,
                              double lr, double rho, hipStream_t stream);

@@ -47,6 +47,12 @@
 
 #include <algorithm>
 
+// Compiled once per range of worker counts (EDIT_K_RANGES); the build passes
+// the range's first and last K.
+#if !defined(EDIT_K_FIRST) || !defined(EDIT_K_LAST)
+#error "compile with -DEDIT_K_FIRST=<first K> -DEDIT_K_LAST=<last K> of one of EDIT_K_RANGES"
+#endif
+
 namespace edit {
 namespace {
 
@@ -164,6 +170,20 @@ __device__ __forceinline__ u32x4 pack(const float (&x)[Vec<BF16>::VE]) {
 template <bool BF16>
 __device__ __forceinline__ double delta64(const u32x4& raw, int e, float th) {
   return static_cast<double>(element<BF16>(raw, e)) - static_cast<double>(th);
+}
+
+// A field of a unit record read by the update pass.  When the record was
+// written earlier in the same launch (the single-block path, kFresh), the
+// load is a relaxed atomic at work-group scope: always a vector memory
+// instruction, which sees the other waves' stores once a barrier has
+// ordered them, whereas a scalar-cache load could return stale data.  A
+// record written by an earlier launch is read with a plain load.
+template <bool kFresh, typename T>
+__device__ __forceinline__ T rec_load(const T* p) {
+  if constexpr (kFresh)
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  else
+    return *p;
 }
 
 // Sum over the 64 lanes of a wave, fixed butterfly order (same in every lane).
@@ -333,14 +353,16 @@ struct PrevDecide {
 };
 
 // Threads per block of the Gram pass.  The MFMA version runs one block per
-// CU holding all its resident waves (3 per SIMD), so the block reduction
+// CU holding all its resident waves (3 per SIMD up to K = 16, 2 above, where
+// the 21 to 36 accumulator tiles and the double-buffered vectors of eight
+// worker groups need up to 256 VGPRs per lane), so the block reduction
 // combines them and the decision reduces one partial row per CU: at K = 16
 // that row count (255 against 767) took the decision from 26 to 12 us.  The
 // VALU version keeps 256-thread blocks: one 512-thread block per CU shortened
 // its decision too, but made the whole 1B step 0.7% slower (same-box A/B).
 template <int K>
 constexpr int pass1_threads() {
-  return K <= 8 ? 256 : 768;
+  return K <= 8 ? 256 : (K <= 16 ? 768 : 512);
 }
 
 template <int K, int kBlockThreads>
@@ -466,15 +488,15 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_pair_kernel(Pas
   }
 }
 
-// Pass 1 for 8 < K <= 16: the Gram matrix sum_i d_i d_i^T over the unit's
-// elements is a rank-n update, and with K(K+1)/2 = 136 fp64 sums per lane a
-// VALU version runs out of registers.  It runs on the fp64 matrix cores as
-// v_mfma_f64_4x4x4f64, four independent 4x4x4 products per wave instruction
-// (blocks b = 0..3).  The workers form G = ceil(K/4) groups of four and the
-// Gram matrix 4x4 tiles (I, J); only the G(G+1)/2 tiles with I <= J are
-// formed (10 of 16 at K = 16): 160 products per element where the 16x16x4
-// instruction forms all 256, and this one also sustains a higher share of
-// the fp64 matrix peak.  On gfx950 the fp64 matrix work and the fp64
+// Pass 1 for 8 < K <= 32: the Gram matrix sum_i d_i d_i^T over the unit's
+// elements is a rank-n update, and with K(K+1)/2 = 136 to 528 fp64 sums per
+// lane a VALU version runs out of registers.  It runs on the fp64 matrix
+// cores as v_mfma_f64_4x4x4f64, four independent 4x4x4 products per wave
+// instruction (blocks b = 0..3).  The workers form G = ceil(K/4) groups of
+// four and the Gram matrix 4x4 tiles (I, J); only the G(G+1)/2 tiles with
+// I <= J are formed (10 of 16 at K = 16, 36 of 64 at K = 32): 160 products
+// per element at K = 16 where the 16x16x4 instruction forms all 256, and
+// this one also sustains a higher share of the fp64 matrix peak.  On gfx950 the fp64 matrix work and the fp64
 // vector work of the deltas (widening, subtracting theta) do not overlap,
 // so the pass is bound by their sum rather than by HBM.
 //
@@ -588,7 +610,7 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_mfma_kernel(con
                                                                    double* __restrict__ partials,
                                                                    PrevDecide prev,
                                                                    DecideParams prm) {
-  static_assert(K > 8 && K <= 16, "MFMA Gram pass covers 8 < K <= 16");
+  static_assert(K > 8 && K <= 32, "MFMA Gram pass covers 8 < K <= 32");
   const int first = prev.partials ? 1 : 0;  // block 0 may take the previous unit's decision
   if (first && blockIdx.x == 0) {
     run_prev_decide<K, pass1_threads<K>()>(prev, prm);
@@ -712,6 +734,7 @@ __global__ __launch_bounds__(kPass2Threads) void pass2_update_kernel(float* __re
   const int64_t v = static_cast<int64_t>(gridDim.x - 1 - blockIdx.x) * kPass2Threads + threadIdx.x;
   const int64_t tail = nvec * VE + threadIdx.x;
   const bool do_tail = blockIdx.x == 0 && tail < n;
+  constexpr bool kRecFresh = false;  // written by the decision of an earlier launch
 
 #include "update_vector_at.inc"
 }
@@ -727,8 +750,9 @@ __global__ __launch_bounds__(kPass2Threads) void pass2_update_kernel(float* __re
 // per thread), included from the same fragments, so the results are the
 // same bit for bit.  The partial row and the record are written and read
 // back within the block: __syncthreads() orders global memory between the
-// waves of one work-group (they share the CU's L1), and the record is read
-// with vector loads (it is written in this kernel).
+// waves of one work-group (they share the CU's L1); the partials are read
+// with non-temporal vector loads and the record with work-group-scope
+// atomic loads (rec_load), never through the scalar cache.
 template <int K>
 struct SingleBlockUnit {
   float* theta;
@@ -781,6 +805,7 @@ __device__ void single_block_unit(const SingleBlockUnit<K>& su, const DecidePara
     const int64_t v = threadIdx.x;
     const int64_t tail = nvec * VE + threadIdx.x;
     const bool do_tail = tail < n;
+    constexpr bool kRecFresh = true;  // written by this block's decision just above
 #include "update_vector_at.inc"
   }
 }
@@ -1124,10 +1149,11 @@ hipError_t pass2_launch(int blocks, float* theta, float* mom, void* const* reps,
 }
 
 // Vectors per thread of the one-pass kernel (measured: two 16-byte vectors
-// of bf16 replicas, one of fp32).
-template <bool BF16>
+// of bf16 replicas, one of fp32; one above K = 16, where two would hold
+// 2K 16-byte registers of replica data per lane).
+template <int K, bool BF16>
 constexpr int fused_v() {
-  return BF16 ? 2 : 1;
+  return BF16 && K <= 16 ? 2 : 1;
 }
 
 template <int K, bool BF16>
@@ -1136,7 +1162,7 @@ hipError_t fused_mean_launch(int rows, float* theta, float* mom, void* const* re
   MutPtrs<K> rp;
   for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
   const int64_t nvec = n / Vec<BF16>::VE;
-  hipLaunchKernelGGL((fused_mean_kernel<K, BF16, kNT2, fused_v<BF16>()>), dim3(rows), dim3(kFusedThreads),
+  hipLaunchKernelGGL((fused_mean_kernel<K, BF16, kNT2, fused_v<K, BF16>()>), dim3(rows), dim3(kFusedThreads),
                      0, stream, theta, mom, rp, partials, rec, nvec, n, lr, rho);
   return hipGetLastError();
 }
@@ -1156,160 +1182,84 @@ int occupancy(Kern kernel, int threads) {
   return blocks;
 }
 
+template <int K>
+struct Launchers {
+  static hipError_t pass1(bool bf16, int rows, const float* theta, const void* const* reps, int64_t n,
+                          double* partials, const double* prev_partials, int prev_rows, UnitRecord* prev_rec,
+                          const DecideParams& prm, hipStream_t stream) {
+    return bf16 ? pass1_launch<K, true>(rows, theta, reps, n, partials, prev_partials, prev_rows, prev_rec, prm,
+                                        stream)
+                : pass1_launch<K, false>(rows, theta, reps, n, partials, prev_partials, prev_rows, prev_rec, prm,
+                                         stream);
+  }
+  static hipError_t pass1_pair(bool bf16, const Pass1Desc* unit, int count, const DecideDesc* prev, int nprev,
+                               const DecideParams& prm, hipStream_t stream) {
+    return bf16 ? pass1_pair_launch<K, true>(unit, count, prev, nprev, prm, stream)
+                : pass1_pair_launch<K, false>(unit, count, prev, nprev, prm, stream);
+  }
+  static hipError_t round_small(bool bf16, const DecideDesc* prev, int nprev, const DecideParams& prm,
+                                const SingleBlockDesc* unit, int count, double lr, double rho,
+                                hipStream_t stream) {
+    return bf16 ? round_small_launch<K, true>(prev, nprev, prm, unit, count, lr, rho, stream)
+                : round_small_launch<K, false>(prev, nprev, prm, unit, count, lr, rho, stream);
+  }
+  static hipError_t pass2(bool bf16, int blocks, float* theta, float* mom, void* const* reps,
+                          const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
+    return bf16 ? pass2_launch<K, true>(blocks, theta, mom, reps, rec, n, lr, rho, stream)
+                : pass2_launch<K, false>(blocks, theta, mom, reps, rec, n, lr, rho, stream);
+  }
+  static hipError_t fused_mean(bool bf16, int rows, float* theta, float* mom, void* const* reps,
+                               double* partials, UnitRecord* rec, int64_t n, double lr, double rho,
+                               hipStream_t stream) {
+    return bf16 ? fused_mean_launch<K, true>(rows, theta, mom, reps, partials, rec, n, lr, rho, stream)
+                : fused_mean_launch<K, false>(rows, theta, mom, reps, partials, rec, n, lr, rho, stream);
+  }
+  static int pass1_blocks_per_cu(bool bf16) {
+    return bf16 ? occupancy(pass1_kernel<K, true>(), pass1_threads<K>())
+                : occupancy(pass1_kernel<K, false>(), pass1_threads<K>());
+  }
+};
+
+// The set of K, or nullptr when K lies outside this object's range (the
+// discarded branch instantiates nothing).
+template <int K>
+const KernelSet* set_if_in_range() {
+  if constexpr (K >= EDIT_K_FIRST && K <= EDIT_K_LAST) {
+    static constexpr KernelSet set{
+        &Launchers<K>::pass1,          &Launchers<K>::pass1_pair,     &Launchers<K>::round_small,
+        &decide_launch<K>,             &gram_reduce_launch<K>,        &decide_gram_launch<K>,
+        &Launchers<K>::pass2,          &Launchers<K>::fused_mean,     &fused_finish_launch<K>,
+        &Launchers<K>::pass1_blocks_per_cu, fused_v<K, true>(),       fused_v<K, false>()};
+    return &set;
+  } else {
+    return nullptr;
+  }
+}
+
 }  // namespace
 
-#define EDIT_FOR_EACH_K(X) \
-  X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16)
+#define EDIT_FOR_EACH_K(X)                                                                       \
+  X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16) X(17)   \
+  X(18) X(19) X(20) X(21) X(22) X(23) X(24) X(25) X(26) X(27) X(28) X(29) X(30) X(31) X(32)
 
-hipError_t launch_pass1(int K, bool bf16, int rows, const float* theta, const void* const* reps,
-                        int64_t n, double* partials, const double* prev_partials, int prev_rows,
-                        UnitRecord* prev_rec, const DecideParams& prm, hipStream_t stream) {
-  switch (K) {
-#define EDIT_CASE(KK)                                                                       \
-  case KK:                                                                                  \
-    return bf16 ? pass1_launch<KK, true>(rows, theta, reps, n, partials, prev_partials,     \
-                                         prev_rows, prev_rec, prm, stream)                  \
-                : pass1_launch<KK, false>(rows, theta, reps, n, partials, prev_partials,    \
-                                          prev_rows, prev_rec, prm, stream);
-    EDIT_FOR_EACH_K(EDIT_CASE)
-#undef EDIT_CASE
-    default:
-      return hipErrorInvalidValue;
-  }
-}
-
-hipError_t launch_pass1_pair(int K, bool bf16, const Pass1Desc* unit, int count, const DecideDesc* prev,
-                             int nprev, const DecideParams& prm, hipStream_t stream) {
-  if (count < 1 || count > 2 || nprev < 0 || nprev > 2) return hipErrorInvalidValue;
-  switch (K) {
-#define EDIT_CASE(KK)                                                                              \
-  case KK:                                                                                         \
-    return bf16 ? pass1_pair_launch<KK, true>(unit, count, prev, nprev, prm, stream)               \
-                : pass1_pair_launch<KK, false>(unit, count, prev, nprev, prm, stream);
-    EDIT_FOR_EACH_K(EDIT_CASE)
-#undef EDIT_CASE
-    default:
-      return hipErrorInvalidValue;
-  }
-}
-
-hipError_t launch_round_small(int K, bool bf16, const DecideDesc* prev, int nprev, const DecideParams& prm,
-                              const SingleBlockDesc* unit, int count, double lr, double rho,
-                              hipStream_t stream) {
-  if (count < 0 || count > kMaxSingleBlockUnits || nprev < 0 || nprev > 2) return hipErrorInvalidValue;
-  switch (K) {
-#define EDIT_CASE(KK)                                                                              \
-  case KK:                                                                                         \
-    return bf16 ? round_small_launch<KK, true>(prev, nprev, prm, unit, count, lr, rho, stream)     \
-                : round_small_launch<KK, false>(prev, nprev, prm, unit, count, lr, rho, stream);
-    EDIT_FOR_EACH_K(EDIT_CASE)
-#undef EDIT_CASE
-    default:
-      return hipErrorInvalidValue;
-  }
-}
-
-hipError_t launch_decide(int K, const double* partials, int rows, UnitRecord* rec,
-                         const DecideParams& prm, hipStream_t stream) {
+const KernelSet* EDIT_KERNEL_SET_FN(EDIT_K_FIRST)(int K) {
   switch (K) {
 #define EDIT_CASE(KK) \
   case KK:            \
-    return decide_launch<KK>(partials, rows, rec, prm, stream);
+    return set_if_in_range<KK>();
     EDIT_FOR_EACH_K(EDIT_CASE)
 #undef EDIT_CASE
     default:
-      return hipErrorInvalidValue;
+      return nullptr;
   }
 }
 
-hipError_t launch_gram_reduce(int K, const double* partials, int rows, double* gram,
-                              hipStream_t stream) {
-  switch (K) {
-#define EDIT_CASE(KK) \
-  case KK:            \
-    return gram_reduce_launch<KK>(partials, rows, gram, stream);
-    EDIT_FOR_EACH_K(EDIT_CASE)
-#undef EDIT_CASE
-    default:
-      return hipErrorInvalidValue;
-  }
-}
-
-hipError_t launch_decide_gram(int K, const double* gram, UnitRecord* rec, const DecideParams& prm,
-                              hipStream_t stream) {
-  switch (K) {
-#define EDIT_CASE(KK) \
-  case KK:            \
-    return decide_gram_launch<KK>(gram, rec, prm, stream);
-    EDIT_FOR_EACH_K(EDIT_CASE)
-#undef EDIT_CASE
-    default:
-      return hipErrorInvalidValue;
-  }
-}
-
-hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom, void* const* reps,
-                        const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
-  switch (K) {
-#define EDIT_CASE(KK)                                                                          \
-  case KK:                                                                                     \
-    return bf16 ? pass2_launch<KK, true>(blocks, theta, mom, reps, rec, n, lr, rho, stream)    \
-                : pass2_launch<KK, false>(blocks, theta, mom, reps, rec, n, lr, rho, stream);
-    EDIT_FOR_EACH_K(EDIT_CASE)
-#undef EDIT_CASE
-    default:
-      return hipErrorInvalidValue;
-  }
-}
-
-int fused_vectors_per_thread(bool bf16) { return bf16 ? fused_v<true>() : fused_v<false>(); }
-
-hipError_t launch_fused_mean(int K, bool bf16, int rows, float* theta, float* mom, void* const* reps,
-                             double* partials, UnitRecord* rec, int64_t n, double lr, double rho,
-                             hipStream_t stream) {
-  switch (K) {
-#define EDIT_CASE(KK)                                                                              \
-  case KK:                                                                                         \
-    return bf16 ? fused_mean_launch<KK, true>(rows, theta, mom, reps, partials, rec, n, lr, rho,   \
-                                              stream)                                              \
-                : fused_mean_launch<KK, false>(rows, theta, mom, reps, partials, rec, n, lr, rho,  \
-                                               stream);
-    EDIT_FOR_EACH_K(EDIT_CASE)
-#undef EDIT_CASE
-    default:
-      return hipErrorInvalidValue;
-  }
-}
-
-hipError_t launch_fused_finish(int K, const FinishEntry* table, int units, hipStream_t stream) {
-  switch (K) {
-#define EDIT_CASE(KK) \
-  case KK:            \
-    return fused_finish_launch<KK>(table, units, stream);
-    EDIT_FOR_EACH_K(EDIT_CASE)
-#undef EDIT_CASE
-    default:
-      return hipErrorInvalidValue;
-  }
-}
-
+#if EDIT_K_FIRST == 1  // the copy probe is compiled into one object only
 hipError_t launch_copy(void* dst, const void* src, int64_t nbytes, int blocks, hipStream_t stream) {
   hipLaunchKernelGGL((copy_kernel<kUnrollCopy, kNTCopy>), dim3(blocks), dim3(kThreads), 0, stream,
                      reinterpret_cast<u32x4*>(dst), reinterpret_cast<const u32x4*>(src), nbytes / 16);
   return hipGetLastError();
 }
-
-int pass1_blocks_per_cu(int K, bool bf16) {
-  switch (K) {
-#define EDIT_CASE(KK)                                                          \
-  case KK:                                                                     \
-    return bf16 ? occupancy(pass1_kernel<KK, true>(), pass1_threads<KK>())       \
-                : occupancy(pass1_kernel<KK, false>(), pass1_threads<KK>());
-    EDIT_FOR_EACH_K(EDIT_CASE)
-#undef EDIT_CASE
-    default:
-      return 1;
-  }
-}
+#endif
 
 }  // namespace edit

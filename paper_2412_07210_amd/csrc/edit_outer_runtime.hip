@@ -180,6 +180,20 @@ edit_status_t validate_config(const edit_outer_config_t* cfg) {
       !std::isfinite(cfg->z_threshold))
     return fail(EDIT_EINVAL, "outer_lr, momentum and z_threshold must be finite");
   if (cfg->ema_warmup_rounds < 0) return fail(EDIT_EINVAL, "ema_warmup_rounds must be >= 0");
+  if (cfg->flags & EDIT_AE) {
+    const int64_t w_min = edit_outer_min_warmup(cfg->ema_alpha, cfg->z_threshold);
+    if (w_min < 0)
+      return fail(EDIT_EINVAL, "z_threshold must be > 0 with EDIT_AE: no EMA warm-up lets a worker "
+                               "with a steady norm pass the z-test");
+    if (cfg->ema_warmup_rounds < w_min) {
+      char msg[200];
+      std::snprintf(msg, sizeof msg,
+                    "ema_warmup_rounds must be >= %lld for ema_alpha = %g and z_threshold = %g: a "
+                    "shorter warm-up flags every worker with a steady norm for good",
+                    static_cast<long long>(w_min), cfg->ema_alpha, cfg->z_threshold);
+      return fail(EDIT_EINVAL, msg);
+    }
+  }
   for (int l = 0; l < cfg->num_layers; ++l)
     if (cfg->layer_numel[l] < 0)
       return fail(EDIT_EINVAL, "layer_numel[" + std::to_string(l) + "] is negative");
@@ -204,6 +218,25 @@ edit_status_t current_gfx950(int* device, int* num_cu) {
 }  // namespace edit
 
 extern "C" {
+
+// The z-test of Eq. 1 against the EMA state after k updates by a norm that
+// stays G every round, from the zero state: mu_k = G(1 - (1-alpha)^k) lags
+// G, so a clean worker passes only once k is large enough.  The recurrence
+// is homogeneous in G, so G = 1 stands for every G > 0.
+int64_t edit_outer_min_warmup(double alpha, double delta) {
+  if (!(alpha > 0.0 && alpha <= 1.0) || !std::isfinite(delta)) return -1;
+  constexpr int64_t kSearch = 1 << 20;  // z falls like (1-alpha)^(k/2): far beyond any alpha in use
+  const double G = 1.0;
+  double mu = 0.0, sigma = 0.0;
+  for (int64_t k = 0; k <= kSearch; ++k) {
+    if (!((G - mu) > delta * sigma)) return k;
+    const double m = alpha * G + (1.0 - alpha) * mu;
+    const double dev = G - m;
+    sigma = std::sqrt((1.0 - alpha) * sigma * sigma + alpha * dev * dev);
+    mu = m;
+  }
+  return -1;
+}
 
 const char* edit_outer_strerror(edit_status_t s) {
   switch (s) {
@@ -264,7 +297,7 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
     u.blocks2 = static_cast<int>(std::max<int64_t>(1, ceil_div(nvec, kPass2Threads)));
     if (h->one_pass)
       u.rows = static_cast<int>(std::max<int64_t>(
-          1, ceil_div(nvec, int64_t(kFusedThreads) * fused_vectors_per_thread(bf16))));
+          1, ceil_div(nvec, int64_t(kFusedThreads) * fused_vectors_per_thread(K, bf16))));
     offs[l] = total;
     const size_t per_row = h->one_pass ? size_t(K + 1) : size_t(num_pairs(K));
     const size_t part_bytes = (per_row * u.rows * sizeof(double) + 255) & ~size_t(255);

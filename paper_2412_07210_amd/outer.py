@@ -19,7 +19,7 @@ import torch
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIBRARY = os.path.join(PKG, "libedit_outer.so")
 
-MAX_K = 16
+MAX_K = 32
 AE, WA, GC = 1, 2, 4
 ONE_PASS = 8  # single-pass mean step; only with AE, WA and GC clear
 F32, BF16 = 0, 1
@@ -28,7 +28,7 @@ EDIT_OK, EDIT_EINVAL, EDIT_ENOMEM, EDIT_EHIP, EDIT_ESTATE, EDIT_ENODEV = 0, -1, 
 
 # Every function the header declares; the CPU tests check the library exports them.
 EXPORTS = (
-    "edit_outer_init", "edit_outer_step_layer", "edit_outer_step_round",
+    "edit_outer_init", "edit_outer_min_warmup", "edit_outer_step_layer", "edit_outer_step_round",
     "edit_outer_step_round_host", "edit_outer_gram_layer", "edit_outer_apply_layer",
     "edit_outer_state_get", "edit_outer_state_set",
     "edit_outer_destroy", "edit_outer_strerror", "edit_outer_last_error",
@@ -94,6 +94,8 @@ def load_library() -> ctypes.CDLL:
     vp = ctypes.c_void_p
     lib.edit_outer_init.argtypes = [ctypes.POINTER(_Config), ctypes.POINTER(vp)]
     lib.edit_outer_init.restype = st
+    lib.edit_outer_min_warmup.argtypes = [ctypes.c_double, ctypes.c_double]
+    lib.edit_outer_min_warmup.restype = ctypes.c_int64
     lib.edit_outer_step_layer.argtypes = [vp, ctypes.c_int32, vp, vp, ctypes.POINTER(vp), vp]
     lib.edit_outer_step_layer.restype = st
     lib.edit_outer_step_round.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
@@ -148,6 +150,12 @@ def _check(status: int, what: str) -> None:
         msg = lib.edit_outer_last_error().decode(errors="replace")
         name = lib.edit_outer_strerror(status).decode()
         raise EditOuterError(status, f"{what}: {name}: {msg}")
+
+
+def min_warmup(ema_alpha: float = 0.02, z_threshold: float = 3.0) -> int:
+    """Shortest EMA warm-up (rounds) the library accepts with anomaly
+    elimination on (edit_outer_min_warmup; -1 if none does)."""
+    return int(load_library().edit_outer_min_warmup(float(ema_alpha), float(z_threshold)))
 
 
 def _stream_handle(stream: Optional[torch.cuda.Stream], device: torch.device) -> int:

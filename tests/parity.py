@@ -39,6 +39,18 @@ class NearTie(Exception):
     pass
 
 
+def steady_ema(wl: Workload, n: int, round_: int):
+    """An EMA state (mu_j, sigma_j, round) as a long warm-up at this
+    workload's noise level leaves it, set identically on both sides so that
+    a case can start after the warm-up without paying for it: mu = 1.25 G and
+    sigma = 0.45 G, G = delta_std * sqrt(n) the typical norm of an n-element
+    pseudo gradient.  A clean worker (scale at most 2) passes the z-test
+    (G_j - mu <= 1.35 G) and a x20 or larger one fails it."""
+    G = wl.delta_std * math.sqrt(max(n, 1))
+    K = wl.num_workers
+    return (np.full(K, 1.25 * G), np.full(K, 0.45 * G), round_)
+
+
 def host_bits(t: torch.Tensor) -> np.ndarray:
     """Device tensor -> host numpy (bf16 as uint16 bit patterns)."""
     if t.dtype == torch.bfloat16:

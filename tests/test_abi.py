@@ -1,6 +1,7 @@
 """CPU-side checks of the C-ABI library: it loads, exports every symbol the
 header declares, and rejects bad configurations before touching a GPU."""
 import ctypes
+import math
 import os
 import re
 
@@ -40,8 +41,9 @@ def test_struct_layouts():
     assert ctypes.sizeof(outer._Config) == 4 + 4 + 8 + 4 + 4 + 6 * 8 + 8
     assert outer._Config.layer_numel.offset == 8
     assert outer._LayerState.ema_mean.offset == 24
-    assert outer._LayerState.anomalous.offset == 24 + 4 * 16 * 8
-    assert outer._LayerState.synced_norm.offset == 24 + 4 * 16 * 8 + 16
+    assert outer.MAX_K == 32
+    assert outer._LayerState.anomalous.offset == 24 + 4 * 32 * 8
+    assert outer._LayerState.synced_norm.offset == 24 + 4 * 32 * 8 + 32
 
 
 def test_strerror():
@@ -71,7 +73,7 @@ def _init(**over):
 
 @pytest.mark.parametrize("over,needle", [
     (dict(num_workers=0), "num_workers"),
-    (dict(num_workers=17), "num_workers"),
+    (dict(num_workers=33), "num_workers"),
     (dict(num_layers=0), "num_layers"),
     (dict(replica_dtype=7), "replica_dtype"),
     (dict(flags=16), "flag"),
@@ -83,6 +85,11 @@ def _init(**over):
     (dict(clip_threshold=-1.0), "clip_threshold"),
     (dict(outer_lr=float("nan")), "finite"),
     (dict(ema_warmup_rounds=-1), "warmup"),
+    (dict(ema_warmup_rounds=5), "ema_warmup_rounds must be >= 6"),
+    (dict(ema_warmup_rounds=0), "ema_warmup_rounds must be >= 6"),
+    (dict(ema_alpha=0.005, ema_warmup_rounds=10), "ema_warmup_rounds must be >= 22"),
+    (dict(z_threshold=0.0), "z_threshold must be > 0"),
+    (dict(z_threshold=-1.0), "z_threshold must be > 0"),
     (dict(numel=[10, -1]), "negative"),
 ])
 def test_init_rejects_bad_config(over, needle):
@@ -95,7 +102,8 @@ def test_init_rejects_bad_config(over, needle):
     (dict(rank=-1), "rank"),
     (dict(rank=4), "rank"),
     (dict(rank=0, flags=8), "EDIT_ONE_PASS"),
-    (dict(rank=0, num_workers=17), "num_workers"),
+    (dict(rank=0, num_workers=33), "num_workers"),
+    (dict(rank=0, ema_warmup_rounds=2), "ema_warmup_rounds must be >= 6"),
     (dict(rank=0, ema_alpha=0.0), "ema_alpha"),
     (dict(rank=1, numel=[5, -2]), "negative"),
 ])
@@ -104,6 +112,50 @@ def test_group_init_rejects_bad_config(over, needle):
     rc, msg = _init(**over)
     assert rc == outer.EDIT_EINVAL
     assert needle in msg
+
+
+@pytest.mark.parametrize("over", [
+    dict(ema_warmup_rounds=6),                   # the paper's alpha and delta: 6 rounds suffice
+    dict(flags=0, ema_warmup_rounds=0),          # no anomaly elimination: no warm-up needed
+    dict(flags=6, ema_warmup_rounds=0, z_threshold=0.0),
+    dict(num_workers=32),
+])
+def test_init_accepts_config(over):
+    """Accepted configurations get past validation (here, without a GPU, the
+    device check then fails instead)."""
+    rc, msg = _init(**over)
+    assert rc != outer.EDIT_EINVAL, msg
+
+
+def _closed_form_z(alpha, k):
+    """z-score of a worker whose norm G never changes, against the EMA of
+    Eq. 1 after k updates from zero: mu_k = G(1 - (1-alpha)^k) and
+    sigma_k = G (1-alpha)^((k+1)/2) sqrt(1 - (1-alpha)^k) (closed form of the
+    recurrence, independent of the library's iteration)."""
+    a = 1.0 - alpha
+    return a ** ((k - 1) / 2) / math.sqrt(1.0 - a ** k)
+
+
+@pytest.mark.parametrize("alpha,delta", [(0.02, 3.0), (0.02, 2.0), (0.02, 5.0), (0.1, 3.0), (0.005, 3.0),
+                                         (0.3, 1.5)])
+def test_min_warmup_matches_closed_form(alpha, delta):
+    """edit_outer_min_warmup is the first k whose closed-form z-score is at
+    most delta (the z-test flags G - mu > delta sigma)."""
+    k = 1
+    while _closed_form_z(alpha, k) > delta:
+        k += 1
+    assert outer.min_warmup(alpha, delta) == k
+    # the paper's alpha = 0.02 and delta = 3 (Sec. 3.2)
+    assert outer.min_warmup() == 6
+    assert _closed_form_z(0.02, 5) > 3.0 > _closed_form_z(0.02, 6)
+
+
+def test_min_warmup_rejects_impossible():
+    assert outer.min_warmup(0.02, 0.0) == -1
+    assert outer.min_warmup(0.02, -2.0) == -1
+    assert outer.min_warmup(0.0, 3.0) == -1
+    assert outer.min_warmup(1.5, 3.0) == -1
+    assert outer.min_warmup(0.02, float("nan")) == -1
 
 
 def test_null_arguments_are_rejected():

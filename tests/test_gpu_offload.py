@@ -35,12 +35,11 @@ def test_host_round_matches_resident_round(K, dtype, one_pass):
     non-index order, three rounds: theta, b, replicas and records equal the
     resident round's bit for bit."""
     sizes = [1_000_000, 2048, 7, 3_000_017, 0, 65_536 + 3]
-    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype, warmup_rounds=1,
-                     name=f"host{K}{dtype}")
+    wl = synth.small("llama1b-k8-bf16", sizes, num_workers=K, replica_dtype=dtype, name=f"host{K}{dtype}")
     order = [2, 0, 5, 1, 4, 3]
     flags = {"flags": ONE_PASS} if one_pass else {}
-    dev_h = EditOuter(OuterConfig(K, wl.layer_numel, dtype, ema_warmup_rounds=1, **flags), DEV)
-    host_h = EditOuter(OuterConfig(K, wl.layer_numel, dtype, ema_warmup_rounds=1, **flags), DEV)
+    dev_h = EditOuter(OuterConfig(K, wl.layer_numel, dtype, **flags), DEV)
+    host_h = EditOuter(OuterConfig(K, wl.layer_numel, dtype, **flags), DEV)
     dev_units = [_inputs(wl, u, 0) for u in range(wl.num_units)]
     host_units = []
     for th, b, reps in dev_units:
@@ -78,13 +77,12 @@ def test_host_round_matches_resident_round(K, dtype, one_pass):
 def test_host_round_matches_oracle():
     """Two units, three rounds against the oracle: two warm-up rounds, then,
     from a preset post-warm-up EMA state on both sides, a round in which
-    worker 1 is x40 and must be masked.  Each round both sides start from the
-    oracle's theta and b (byte-identical inputs)."""
-    wl = synth.small("llama1b-k8-bf16", [300_001, 4099], num_workers=5, replica_dtype="bf16", warmup_rounds=2,
+    worker 1 is x40 and must be masked while the others pass.  Each round
+    both sides start from the oracle's theta and b (byte-identical inputs)."""
+    wl = synth.small("llama1b-k8-bf16", [300_001, 4099], num_workers=5, replica_dtype="bf16",
                      clip_threshold=0.2, name="hostpar")
-    K = wl.num_workers
-    lib = EditOuter(OuterConfig(K, wl.layer_numel, "bf16", ema_warmup_rounds=2,
-                                clip_threshold=0.2), DEV)
+    K, W = wl.num_workers, wl.warmup_rounds
+    lib = EditOuter(OuterConfig(K, wl.layer_numel, "bf16", ema_warmup_rounds=W, clip_threshold=0.2), DEV)
     oracles = [OracleUnit(K, OracleConfig(**wl.hyper())) for _ in range(2)]
     th_h = [wl.init_theta(u, DEV).cpu().pin_memory() for u in range(2)]
     b_h = [torch.zeros(wl.unit_numel(u), dtype=torch.float32).pin_memory() for u in range(2)]
@@ -94,13 +92,13 @@ def test_host_round_matches_oracle():
             for u in range(2)]
     try:
         plan = lib.prepare_round([(th_h[u], b_h[u], reps[u]) for u in range(2)], host=True)
-        for t in range(3):
-            std = wl.worker_std(t) * (np.where(np.arange(K) == 1, 40.0, 1.0) if t == 2 else 1.0)
+        for t in (0, 1, W):
+            std = wl.worker_std(t) * (np.where(np.arange(K) == 1, 40.0, 1.0) if t == W else 1.0)
             reps_h = []
             for u in range(2):
-                if t == 2:
+                if t == W:
                     G0 = wl.delta_std * np.sqrt(wl.unit_numel(u))
-                    ema = (np.full(K, 1.25 * G0), np.full(K, 0.45 * G0), 2)
+                    ema = (np.full(K, 1.25 * G0), np.full(K, 0.45 * G0), W)
                     oracles[u].set_state(*ema)
                     lib.state_set(u, *ema)
                 th_h[u].copy_(torch.from_numpy(o_th[u]))
@@ -116,7 +114,7 @@ def test_host_round_matches_oracle():
                 compare_decision(lib.state_get(u), recs[u], K, what)
                 assert_tensor_close(th_h[u].numpy(), o_th[u], what + ": theta")
                 assert_tensor_close(b_h[u].numpy(), o_b[u], what + ": momentum")
-            if t == 2:
+            if t == W:
                 assert [list(r["anomalous"]) for r in recs] == [[0, 1, 0, 0, 0]] * 2
     finally:
         lib.close()

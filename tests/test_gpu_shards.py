@@ -45,9 +45,10 @@ def _preset_ema(wl, n):
     return (np.full(K, 1.25 * G), np.full(K, 0.45 * G), wl.warmup_rounds)
 
 
-def _sharded_rounds(wl, shards, rounds, ema=None, verbose=True):
+def _sharded_rounds(wl, shards, rounds, ema=None, verbose=True, scale=None):
     """Lock-step: oracle on the whole module, library on its shards.  `ema`
-    maps a round to the EMA state both sides take before that round."""
+    maps a round to the EMA state both sides take before that round, `scale`
+    a round to a factor on every worker's pseudo gradient."""
     K, bf16 = wl.num_workers, wl.replica_dtype == "bf16"
     n = wl.unit_numel(0)
     assert sum(shards) == n
@@ -66,7 +67,7 @@ def _sharded_rounds(wl, shards, rounds, ema=None, verbose=True):
                     lib.state_set(s, *ema[t])
             theta = torch.from_numpy(theta_h).to(DEV)
             reps = [torch.empty(n, dtype=wl.torch_dtype, device=DEV) for _ in range(K)]
-            wl.fill_replicas(theta, reps, 0, t)
+            wl.fill_replicas(theta, reps, 0, t, std=wl.worker_std(t) * (scale or {}).get(t, 1.0))
             reps_h = [host_bits(r) for r in reps]
             # each shard in buffers of its own (16-byte aligned, as a device would hold them)
             th_s = [theta[a:b].clone() for a, b in zip(cuts[:-1], cuts[1:])]
@@ -125,13 +126,15 @@ def test_sharded_module_matches_unsplit_oracle(K, dtype, shards):
 
 
 def test_sharded_module_rollback_and_clip():
-    """phi small enough to clip; with a one-round warm-up from the zero EMA
-    state every worker fails the next z-test, so round 1 rolls back on the
-    module norm (and round 2, the state being unchanged, again)."""
+    """phi small enough to clip in a warm-up round; after the warm-up, from a
+    settled EMA state, every worker x100: all fail the z-test on the module
+    norm and the module rolls back (twice, the state being unchanged)."""
     wl = synth.small("linear1m-k4", [65536 + 4099], num_workers=4, replica_dtype="bf16",
-                     warmup_rounds=1, clip_threshold=1e-3)
+                     clip_threshold=1e-3)
+    W = wl.warmup_rounds
     try:
-        recs = list(_sharded_rounds(wl, (65536, 4099), range(3)))
+        recs = list(_sharded_rounds(wl, (65536, 4099), [0, W, W + 1],
+                                    ema={W: _preset_ema(wl, 65536 + 4099)}, scale={W: 100.0, W + 1: 100.0}))
     except NearTie as e:
         pytest.skip(str(e))
     assert recs[0]["clip_coef"] < 1.0 and not recs[0]["rolled_back"]

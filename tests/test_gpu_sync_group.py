@@ -149,15 +149,15 @@ def test_group_matches_the_full_step(K, dtype, n):
 
 
 def test_group_rollback_and_clip():
-    """A one-round warm-up from the zero EMA state: every worker fails the
-    next z-test, so round 1 rolls back on every rank; phi small enough to clip
-    in round 0."""
-    wl = synth.small("linear1m-k4", [70_001], num_workers=4, replica_dtype="bf16", warmup_rounds=1,
-                     clip_threshold=1e-3)
-    g = Group(wl, 70_001)
+    """phi small enough to clip in a warm-up round; after the warm-up, from a
+    settled EMA state, every worker x100 fails its own z-test, so the round
+    rolls back on every rank."""
+    wl = synth.small("linear1m-k4", [70_001], num_workers=4, replica_dtype="bf16", clip_threshold=1e-3)
+    W = wl.warmup_rounds
+    g = Group(wl, 70_001, ema={W: _preset(wl, 70_001, 4)})
     try:
         r0, _ = g.round(0)
-        r1, states = g.round(1)
+        r1, states = g.round(W, std=wl.worker_std(W) * 100.0)
     finally:
         g.close()
     assert r0["clip_coef"] < 1.0 and not r0["rolled_back"]
