@@ -143,35 +143,194 @@ def host_link_probe_gbps(torch, nbytes: int = 1 << 30, reps: int = 3) -> dict:
     return out
 
 
-def cpu_baseline(samples, wl, seconds_hint: float, one_pass: bool = False):
-    """Time the CPU oracle (one thread, as it stands) on the captured units;
-    for the one-pass mode, the oracle with every penalty component off."""
+def update_probe(torch, lib, units, wl, reps: int, roofline: dict) -> dict:
+    """Each unit's update-pass traffic with no arithmetic
+    (edit_outer_update_probe: the update pass's grid and 16-byte loads and
+    stores of theta, b and all K replicas, values written back unchanged),
+    each launch timed with HIP events on the current stream, against the
+    update pass's own sampled launches of the timed rounds."""
+    K, R = wl.num_workers, wl.replica_bytes
+    ve = 16 // R
+    ms, nbytes = [], []
+    for _ in range(reps):
+        for u, (th, b, rp) in enumerate(units):
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            lib.update_probe(u, th, b, rp)
+            z.record()
+            torch.cuda.synchronize()
+            ms.append(a.elapsed_time(z))
+            nbytes.append((th.numel() // ve) * ve * (16 + 2 * K * R))
+    avg = sum(ms) / len(ms)
+    gbps = sum(nbytes) / len(nbytes) / (avg * 1e-3) / 1e9
+    return {
+        "kernel": "update_pattern_probe_kernel (the update pass's loads and stores, no arithmetic)",
+        "avg_launch_ms": round(avg, 5), "gbps": round(gbps, 2), "frac": round(gbps / PEAK_HBM_GBPS, 4),
+        "bytes_per_launch": int(sum(nbytes) / len(nbytes)), "launches": len(ms),
+        "update_pass_avg_launch_ms": roofline["avg_launch_ms"],
+        "update_pass_over_probe_time": round(roofline["avg_launch_ms"] / avg, 4),
+    }
+
+
+def host_cpu() -> dict:
+    """The host's CPU model (as lscpu reports it) and the cores this process
+    may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"model": model, "affinity_cores": len(os.sched_getaffinity(0))}
+
+
+def oracle_threads() -> int:
+    """Threads for the CPU baseline: every core in the affinity mask, capped
+    by OMP_NUM_THREADS when the environment sets it (the host's share)."""
+    n = len(os.sched_getaffinity(0))
+    cap = os.environ.get("OMP_NUM_THREADS", "")
+    return max(1, min(n, int(cap))) if cap.isdigit() and int(cap) > 0 else max(1, n)
+
+
+def cpu_baseline(samples, wl, one_pass: bool = False):
+    """Time the CPU oracle (as it stands: one thread per unit step) on every
+    unit of one captured round.  First one unit alone on one thread, then all
+    units at once, one per thread on every core of the host's share (the
+    units are independent; each unit's step is unchanged).  For the one-pass
+    mode, the oracle with every penalty component off."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import numpy as np
     from oracle import OracleConfig, OracleUnit
 
     K, R = wl.num_workers, wl.replica_bytes
-    total_bytes, total_s, done = 0, 0.0, 0
-    for (u, theta, mom, reps) in samples:
-        unit = OracleUnit(K, OracleConfig(**wl.hyper(), **({"flags": 0} if one_pass else {})))
-        t0 = time.perf_counter()
-        unit.step(theta, mom, reps)
-        dt = time.perf_counter() - t0
-        total_s += dt
-        total_bytes += theta.size * ((2 * K * R + 16) if one_pass else (3 * K * R + 20))
-        done += 1
-        log(f"cpu oracle unit {u}: {dt:.2f} s")
-        if total_s > seconds_hint:
-            break
-    per_unit_s = total_s / done
+    cfg = OracleConfig(**wl.hyper(), **({"flags": 0} if one_pass else {}))
+    per_elt = (2 * K * R + 16) if one_pass else (3 * K * R + 20)
+    total_bytes = sum(th.size for (_, th, _, _) in samples) * per_elt
+    # one unit, one thread (on a copy: the all-core run below steps every unit in place)
+    u0, th0, b0, reps0 = samples[0]
+    t0 = time.perf_counter()
+    OracleUnit(K, cfg).step(th0.copy(), b0.copy(), [r.copy() for r in reps0])
+    one_s = time.perf_counter() - t0
+    log(f"cpu oracle, one thread: unit {u0} in {one_s:.2f} s")
+    threads = oracle_threads()
+
+    def step(sample):
+        _, th, b, reps = sample
+        OracleUnit(K, cfg).step(th, b, reps)
+
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(threads) as pool:
+        list(pool.map(step, samples))
+    all_s = time.perf_counter() - t0
+    log(f"cpu oracle, {threads} threads: {len(samples)} units in {all_s:.2f} s")
+    n0 = samples[0][1].size
     return {
-        "value": round(total_bytes / total_s / 1e9, 4),
+        "value": round(total_bytes / all_s / 1e9, 4),
         "unit": "GB/s",
-        "cores": 1,
+        "cores": threads,
         "kind": "oracle",
-        "ms_per_step_extrapolated": round(per_unit_s * wl.num_units * 1e3, 1),
-        "sample": f"{done} of {wl.num_units} units of one round ({samples[0][1].size:,} elements each, "
-                  f"K={K}), single-threaded C oracle, fp64",
+        "ms_per_step": round(all_s * 1e3, 1),
+        "one_thread_ms_per_unit": round(one_s * 1e3, 1),
+        "one_thread_ms_per_step": round(one_s * 1e3 * len(samples), 1),
+        "host_cpu": host_cpu(),
+        "sample": f"all {len(samples)} units of one round ({n0:,} elements each, K={K}) stepped by the "
+                  f"C oracle (fp64) one unit per thread on {threads} threads: ms_per_step and value are "
+                  f"that run's wall time; one_thread_* is one unit alone on one thread (times "
+                  f"{len(samples)} for a step)",
     }
+
+
+# The other single-GPU workloads, measured after the headline in the same run
+# (the 1024x1024 layer fits the Infinity Cache and is latency-bound: a parity
+# case, not a bandwidth line).
+SECONDARY = ("llama350m-k8-f32", "llama7b-half-k8-bf16", "aedit1b-k16-bf16")
+
+
+def measure_secondary(torch, np, name: str, steps: int, warmup: int, seed: int, dev, profile_every: int = 12):
+    """One workload's rounds through edit_outer_step_round, as the headline
+    (fresh handle and inputs, cache settle before each round, HIP events on
+    every `profile_every`-th unit): ms/step percentiles, GB/s of the design
+    bytes and the sampled kernels' rooflines.  Frees everything it made."""
+    from paper_2412_07210_amd import EditOuter, OuterConfig, outer, synth
+
+    wl = synth.get(name)
+    K, R = wl.num_workers, wl.replica_bytes
+    hyper = wl.hyper()
+    warm = hyper.pop("warmup_rounds")
+    lib = EditOuter(OuterConfig(num_workers=K, layer_numel=wl.layer_numel, replica_dtype=wl.replica_dtype,
+                                ema_warmup_rounds=warm, **hyper), dev)
+    units = []
+    for u in range(wl.num_units):
+        th = wl.init_theta(u, dev, seed)
+        units.append((th, torch.zeros_like(th), [torch.empty(th.numel(), dtype=wl.torch_dtype, device=dev)
+                                                 for _ in range(K)]))
+    plan = lib.prepare_round(units)
+    lib.set_profiling(profile_every)
+    settle_src = torch.zeros(256 << 20, dtype=torch.float32, device=dev)
+    settle_dst = torch.empty_like(settle_src)
+    step_ms, p1, p2 = [], [], []  # p1/p2: (ms, algorithmic bytes) of sampled launches
+    step_bytes = min_bytes = 0
+    masked = rollbacks = 0
+    for t in range(warmup + steps):
+        std = wl.worker_std(t, seed)
+        for u, (th, _, reps) in enumerate(units):
+            wl.fill_replicas(th, reps, u, t, seed, std=std)
+        outer.copy_probe(settle_dst, settle_src)
+        torch.cuda.synchronize()
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        plan.run()
+        z.record()
+        torch.cuda.synchronize()
+        if t < warmup:
+            continue
+        step_ms.append(a.elapsed_time(z))
+        for u, (th, _, _) in enumerate(units):
+            st = lib.state_get(u)
+            active = int(np.count_nonzero(st.weight > 0)) if st.clip_coef > 0 else 0
+            b1, b2 = unit_bytes(th.numel(), K, R, active, st.rolled_back)
+            step_bytes += b1 + b2
+            min_bytes += th.numel() * (2 * K * R + 16)
+            masked += int(st.anomalous.sum())
+            rollbacks += int(st.rolled_back)
+            if u % profile_every == 0:
+                k1, k2 = lib.kernel_times(u)
+                p1.append((k1, b1))
+                p2.append((k2, b2))
+    lib.close()
+    del units, plan, settle_src, settle_dst
+    torch.cuda.empty_cache()
+    total_ms = sum(step_ms)
+    q = np.percentile(step_ms, [10, 50, 90])
+    value = step_bytes / (total_ms * 1e-3) / 1e9
+
+    def roof(samples, kernel):
+        ms = sum(m for m, _ in samples) / len(samples)
+        achieved = sum(b for _, b in samples) / len(samples) / (ms * 1e-3) / 1e9
+        return {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4), "avg_launch_ms": round(ms, 5),
+                "sampled_launches": len(samples)}
+
+    pass1_name = "pass1_gram_mfma_kernel" if K > 8 else "pass1_gram_kernel"
+    out = {
+        "workload": f"{wl.name}: {wl.description}", "units": wl.num_units, "num_workers": K,
+        "replica_dtype": wl.replica_dtype, "steps": steps, "warmup": warmup,
+        "ms_per_step": round(total_ms / len(step_ms), 4), "ms_p10": round(float(q[0]), 4),
+        "ms_p50": round(float(q[1]), 4), "ms_p90": round(float(q[2]), 4),
+        "value": round(value, 2), "unit": "GB/s", "pct_peak_hbm": round(100 * value / PEAK_HBM_GBPS, 2),
+        "gbps_on_min_bytes": round(min_bytes / (total_ms * 1e-3) / 1e9, 2),
+        "masked_workers_total": masked, "rollbacks_total": rollbacks,
+        "pass1": roof(p1, pass1_name + " (its unit's Gram pass; in a round up to K = 8 it also "
+                          "carries earlier units' decisions)"),
+        "pass2": roof(p2, "pass2_update_kernel"),
+    }
+    # the dominant kernel by time: the update pass (twice pass 1's bytes)
+    out["dominant"] = "pass2" if sum(m for m, _ in p2) >= sum(m for m, _ in p1) else "pass1"
+    return out
 
 
 # ----------------------------------------------------------------------------
@@ -603,14 +762,19 @@ def main(argv=None) -> int:
     ap.add_argument("--sync-group-rank", type=int, default=None, metavar="R",
                     help="time rank R's share of a sync group whose K replicas sit on K GPUs "
                          "(edit_group_*; the collectives stood in for on the device)")
+    ap.add_argument("--update-probe", type=int, default=3, metavar="REPS",
+                    help="after the timed rounds, time REPS launches per unit of the update pass's access "
+                         "pattern with no arithmetic (edit_outer_update_probe); 0: skip")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--profile-every", type=int, default=12,
                     help="record per-kernel HIP events on every k-th unit (0: none, roofline then null)")
     ap.add_argument("--records", metavar="PATH",
                     help="write every unit's decision of every timed round as JSON lines "
                          "(G, mask, weights, Gbar, beta, EMA state)")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU-baseline time budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--secondary", type=int, default=1,
+                    help="1: after the default workload, also measure " + ", ".join(SECONDARY) + " (0: skip)")
+    ap.add_argument("--secondary-steps", type=int, default=10, help="timed rounds of each secondary workload")
     ap.add_argument("--no-copy-probe", action="store_true")
     ap.add_argument("--no-settle", action="store_true",
                     help="skip the untimed cache settle between input generation and the step")
@@ -740,7 +904,7 @@ def main(argv=None) -> int:
             wl.fill_replicas(th.to(dev) if args.host_state else th, reps, u, t, args.seed, std=std)
         timed = t >= args.warmup
         if timed and t == args.warmup and not args.no_cpu_baseline:
-            for u in range(min(6, wl.num_units)):  # ~14 s of oracle time at the 1B shape
+            for u in range(wl.num_units):  # every unit of the first timed round
                 th, b, reps = units[u]
                 hb = [r.view(torch.int16).cpu().numpy().view(np.uint16) if r.dtype == torch.bfloat16
                       else r.cpu().numpy() for r in reps]
@@ -906,11 +1070,23 @@ def main(argv=None) -> int:
         result["host_link_probe_gbps"] = host_link_probe_gbps(torch)
     if not args.no_copy_probe:
         result["copy_probe_gbps"] = round(copy_probe_gbps(torch, outer), 1)
+    if args.update_probe > 0 and S == 1 and not (args.one_pass or args.host_state) and result.get("roofline"):
+        result["update_probe"] = update_probe(torch, lib, units, wl, args.update_probe, result["roofline"])
     lib.close()
-    del units
+    del units, plan, shard_views
     torch.cuda.empty_cache()
+    if args.secondary and args.config == DEFAULT_WORKLOAD and S == 1 and not (
+            args.one_pass or args.host_state or args.per_unit or args.units):
+        result["secondary"] = {}
+        for name in SECONDARY:
+            t0 = time.time()
+            result["secondary"][name] = measure_secondary(torch, np, name, args.secondary_steps, 10, args.seed,
+                                                          dev)
+            log(f"secondary {name}: {result['secondary'][name]['ms_per_step']} ms/step "
+                f"({time.time() - t0:.1f} s)")
     if samples:
-        result["cpu_baseline"] = cpu_baseline(samples, wl, args.cpu_seconds, args.one_pass)
+        result["cpu_baseline"] = cpu_baseline(samples, wl, args.one_pass)
+        samples.clear()
     print(json.dumps(result), flush=True)
     return 0
 

@@ -335,6 +335,17 @@ edit_status_t edit_outer_set_profiling(edit_outer_t h, int32_t every);
  * reduces all units in one launch at its end).  Waits for it. */
 edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[2]);
 
+/* The memory traffic of unit `layer`'s update pass with no arithmetic: a
+ * kernel with the update pass's grid, block order and 16-byte accesses reads
+ * theta, the momentum and all K replicas and writes them back unchanged
+ * (16 + 2K R bytes per element, the update pass's bytes when every worker
+ * contributes), so its time is the floor this access pattern sets for that
+ * pass.  Elements past the last whole 16-byte replica vector are not
+ * touched.  Arguments and checks as in edit_outer_step_layer; the EMA state
+ * and records are untouched. */
+edit_status_t edit_outer_update_probe(edit_outer_t h, int32_t layer, float *theta, float *momentum,
+                                      void *const *replicas, void *stream);
+
 /* Plain device-to-device copy kernel of nbytes (a multiple of 16, 16-byte
  * aligned, non-overlapping pointers; one 16-byte vector per thread), used to
  * calibrate HBM traffic counters and as the bandwidth reference. */

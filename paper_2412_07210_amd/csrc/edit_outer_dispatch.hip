@@ -80,6 +80,12 @@ hipError_t launch_fused_finish(int K, const FinishEntry* table, int units, hipSt
   return s ? s->fused_finish(table, units, stream) : hipErrorInvalidValue;
 }
 
+hipError_t launch_pattern_probe(int K, bool bf16, int blocks, float* theta, float* mom, void* const* reps,
+                                int64_t n, hipStream_t stream) {
+  const KernelSet* s = kernels_for(K);
+  return s ? s->pattern_probe(bf16, blocks, theta, mom, reps, n, stream) : hipErrorInvalidValue;
+}
+
 int pass1_blocks_per_cu(int K, bool bf16) {
   const KernelSet* s = kernels_for(K);
   return s ? s->pass1_blocks_per_cu(bf16) : 1;

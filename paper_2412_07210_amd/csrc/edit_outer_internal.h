@@ -104,6 +104,8 @@ struct KernelSet {
                            UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream);
   hipError_t (*fused_finish)(const FinishEntry* table, int units, hipStream_t stream);
   int (*pass1_blocks_per_cu)(bool bf16);
+  hipError_t (*pattern_probe)(bool bf16, int blocks, float* theta, float* mom, void* const* reps, int64_t n,
+                              hipStream_t stream);
   int fused_vectors_bf16, fused_vectors_f32;
 };
 
@@ -153,6 +155,9 @@ hipError_t launch_fused_mean(int K, bool bf16, int rows, float* theta, float* mo
 hipError_t launch_fused_finish(int K, const FinishEntry* table, int units, hipStream_t stream);
 hipError_t launch_copy(void* dst, const void* src, int64_t nbytes, int blocks,
                        hipStream_t stream);
+// Pass 2's loads and stores (whole vectors only) with no arithmetic.
+hipError_t launch_pattern_probe(int K, bool bf16, int blocks, float* theta, float* mom, void* const* reps,
+                                int64_t n, hipStream_t stream);
 
 // Resident blocks per CU of the pass-1 kernel (for its persistent grid).
 int pass1_blocks_per_cu(int K, bool bf16);

@@ -739,6 +739,38 @@ __global__ __launch_bounds__(kPass2Threads) void pass2_update_kernel(float* __re
 #include "update_vector_at.inc"
 }
 
+// The access pattern of pass 2 with no arithmetic: the same grid, block
+// order and 16-byte accesses, reading theta, b and all K replicas and
+// writing them all back (XOR with `flip`, zero at run time, keeps every
+// store), so its time is what this traffic costs with nothing computed.
+// Used to calibrate pass 2 against its own pattern, not by the method.
+template <int K, bool BF16, bool NT>
+__global__ __launch_bounds__(kPass2Threads) void update_pattern_probe_kernel(float* __restrict__ theta,
+                                                                            float* __restrict__ mom,
+                                                                            MutPtrs<K> reps, int64_t nvec,
+                                                                            uint32_t flip) {
+  const int64_t v = static_cast<int64_t>(gridDim.x - 1 - blockIdx.x) * kPass2Threads + threadIdx.x;
+  if (v >= nvec) return;
+  constexpr int H = Vec<BF16>::VE / 4;  // 16-byte vectors of theta (and of b) per replica vector
+  u32x4 t[H], b[H], r[K];
+  u32x4* tp = reinterpret_cast<u32x4*>(theta) + v * H;
+  u32x4* bp = reinterpret_cast<u32x4*>(mom) + v * H;
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    t[h] = ld16<NT>(tp + h);
+    b[h] = ld16<NT>(bp + h);
+  }
+#pragma unroll
+  for (int j = 0; j < K; ++j) r[j] = ld16<NT>(reinterpret_cast<const u32x4*>(reps.p[j]) + v);
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    st16<NT>(tp + h, t[h] ^ flip);
+    st16<NT>(bp + h, b[h] ^ flip);
+  }
+#pragma unroll
+  for (int j = 0; j < K; ++j) st16<NT>(reinterpret_cast<u32x4*>(reps.p[j]) + v, r[j] ^ flip);
+}
+
 // ------------------------------------------- single-block units of a round
 
 // A unit whose Gram pass is one block (at most 256 vectors) can be stepped
@@ -1138,6 +1170,17 @@ hipError_t decide_gram_launch(const double* gram, UnitRecord* rec, const DecideP
 }
 
 template <int K, bool BF16>
+hipError_t pattern_probe_launch(int blocks, float* theta, float* mom, void* const* reps, int64_t n,
+                                hipStream_t stream) {
+  MutPtrs<K> rp;
+  for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
+  const int64_t nvec = n / Vec<BF16>::VE;
+  hipLaunchKernelGGL((update_pattern_probe_kernel<K, BF16, kNT2>), dim3(blocks), dim3(kPass2Threads), 0, stream,
+                     theta, mom, rp, nvec, 0u);
+  return hipGetLastError();
+}
+
+template <int K, bool BF16>
 hipError_t pass2_launch(int blocks, float* theta, float* mom, void* const* reps,
                         const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
   MutPtrs<K> rp;
@@ -1208,6 +1251,11 @@ struct Launchers {
     return bf16 ? pass2_launch<K, true>(blocks, theta, mom, reps, rec, n, lr, rho, stream)
                 : pass2_launch<K, false>(blocks, theta, mom, reps, rec, n, lr, rho, stream);
   }
+  static hipError_t pattern_probe(bool bf16, int blocks, float* theta, float* mom, void* const* reps, int64_t n,
+                                  hipStream_t stream) {
+    return bf16 ? pattern_probe_launch<K, true>(blocks, theta, mom, reps, n, stream)
+                : pattern_probe_launch<K, false>(blocks, theta, mom, reps, n, stream);
+  }
   static hipError_t fused_mean(bool bf16, int rows, float* theta, float* mom, void* const* reps,
                                double* partials, UnitRecord* rec, int64_t n, double lr, double rho,
                                hipStream_t stream) {
@@ -1229,7 +1277,8 @@ const KernelSet* set_if_in_range() {
         &Launchers<K>::pass1,          &Launchers<K>::pass1_pair,     &Launchers<K>::round_small,
         &decide_launch<K>,             &gram_reduce_launch<K>,        &decide_gram_launch<K>,
         &Launchers<K>::pass2,          &Launchers<K>::fused_mean,     &fused_finish_launch<K>,
-        &Launchers<K>::pass1_blocks_per_cu, fused_v<K, true>(),       fused_v<K, false>()};
+        &Launchers<K>::pass1_blocks_per_cu, &Launchers<K>::pattern_probe, fused_v<K, true>(),
+        fused_v<K, false>()};
     return &set;
   } else {
     return nullptr;

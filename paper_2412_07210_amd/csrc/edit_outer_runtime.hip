@@ -976,6 +976,18 @@ edit_status_t edit_outer_kernel_times(edit_outer_t h, int32_t layer, float ms[2]
   return EDIT_OK;
 }
 
+edit_status_t edit_outer_update_probe(edit_outer_t h, int32_t layer, float* theta, float* momentum,
+                                      void* const* replicas, void* stream) {
+  if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  EDIT_TRY(check_step(h, layer, theta, momentum, replicas));
+  EDIT_TRY(check_device(h));
+  const Unit& u = h->units[layer];
+  if (u.n == 0) return EDIT_OK;
+  const hipError_t e = launch_pattern_probe(h->cfg.num_workers, h->cfg.replica_dtype == EDIT_BF16, u.blocks2, theta,
+                                            momentum, replicas, u.n, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? EDIT_OK : fail_hip(e, "update probe launch");
+}
+
 edit_status_t edit_outer_copy_probe(void* dst, const void* src, int64_t nbytes, void* stream) {
   if (nbytes < 0 || (nbytes & 15)) return fail(EDIT_EINVAL, "nbytes must be a non-negative multiple of 16");
   if (nbytes == 0) return EDIT_OK;

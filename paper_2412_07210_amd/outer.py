@@ -28,11 +28,12 @@ EDIT_OK, EDIT_EINVAL, EDIT_ENOMEM, EDIT_EHIP, EDIT_ESTATE, EDIT_ENODEV = 0, -1, 
 
 # Every function the header declares; the CPU tests check the library exports them.
 EXPORTS = (
-    "edit_outer_init", "edit_outer_min_warmup", "edit_outer_step_layer", "edit_outer_step_round",
+    "edit_outer_init", "edit_outer_min_warmup", "edit_outer_step_layer",
+    "edit_outer_step_round",
     "edit_outer_step_round_host", "edit_outer_gram_layer", "edit_outer_apply_layer",
     "edit_outer_state_get", "edit_outer_state_set",
     "edit_outer_destroy", "edit_outer_strerror", "edit_outer_last_error",
-    "edit_outer_set_profiling", "edit_outer_kernel_times", "edit_outer_copy_probe",
+    "edit_outer_set_profiling", "edit_outer_kernel_times", "edit_outer_update_probe", "edit_outer_copy_probe",
     "edit_group_init", "edit_group_norm", "edit_group_weights", "edit_group_apply",
     "edit_group_state_get", "edit_group_state_set", "edit_group_destroy",
 )
@@ -124,6 +125,8 @@ def load_library() -> ctypes.CDLL:
     lib.edit_outer_set_profiling.restype = st
     lib.edit_outer_kernel_times.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_float)]
     lib.edit_outer_kernel_times.restype = st
+    lib.edit_outer_update_probe.argtypes = [vp, ctypes.c_int32, vp, vp, ctypes.POINTER(vp), vp]
+    lib.edit_outer_update_probe.restype = st
     lib.edit_outer_copy_probe.argtypes = [vp, vp, ctypes.c_int64, vp]
     lib.edit_outer_copy_probe.restype = st
     lib.edit_group_init.argtypes = [ctypes.POINTER(_Config), ctypes.c_int32, ctypes.POINTER(vp)]
@@ -411,6 +414,14 @@ class EditOuter:
     def set_profiling(self, every: int) -> None:
         """Record kernel events on units l with l % every == 0 (0: off)."""
         _check(self._lib.edit_outer_set_profiling(self._h, int(every)), "set_profiling")
+
+    def update_probe(self, layer: int, theta: torch.Tensor, momentum: torch.Tensor,
+                     replicas: Sequence[torch.Tensor], stream: Optional[torch.cuda.Stream] = None) -> None:
+        """Enqueue unit `layer`'s update-pass traffic with no arithmetic (the
+        tensors are read and written back unchanged)."""
+        ptrs = self._unit_tensors(layer, theta, momentum, replicas)
+        _check(self._call(self._lib.edit_outer_update_probe, int(layer), theta.data_ptr(), momentum.data_ptr(),
+                          ptrs, _stream_handle(stream, self.device)), "edit_outer_update_probe")
 
     def kernel_times(self, layer: int) -> tuple:
         """(pass-1 ms incl. the decision, pass-2 ms) of the unit's last profiled step."""

@@ -103,6 +103,41 @@ def assert_replica_close(gpu: np.ndarray, ref: np.ndarray, bf16: bool, what: str
         assert rel <= BF16_REL_NORM, f"{what}: relative norm error {rel:.3e}"
 
 
+def assert_tensor_close_t(got: torch.Tensor, ref: torch.Tensor, what: str) -> None:
+    """assert_tensor_close on torch tensors (fp32, any one device), in fp64:
+    the same bar, |got - ref| <= 1e-5 (|ref| + rms(ref)) elementwise."""
+    g, r = got.double(), ref.double()
+    assert bool(torch.isfinite(g).all()) == bool(torch.isfinite(r).all()), f"{what}: non-finite mismatch"
+    rms = float(torch.sqrt(torch.mean(r * r))) if r.numel() else 0.0
+    excess = (g - r).abs() - RTOL_F32 * (r.abs() + rms)
+    bad = int((excess > 0).sum())
+    if bad:
+        i = int(torch.argmax(excess))
+        raise AssertionError(f"{what}: {bad} of {r.numel()} elements out of tolerance; worst at {i}: "
+                             f"got {float(g[i])!r} oracle {float(r[i])!r}")
+
+
+def assert_bf16_replica_close_t(got_bits: torch.Tensor, ref_bits: torch.Tensor, what: str) -> None:
+    """assert_replica_close for bf16 replicas given as int16 bit patterns (any
+    one device): every element within one bf16 rounding step plus theta's fp32
+    tolerance of the oracle's, and a relative norm error of at most 2e-3."""
+    g = (got_bits.to(torch.int32) << 16).view(torch.float32).double()
+    r = (ref_bits.to(torch.int32) << 16).view(torch.float32).double()
+    _, e = torch.frexp(r.abs())
+    ulp = torch.where(r == 0, torch.full_like(r, 2.0 ** -133), torch.ldexp(torch.ones_like(r), e - 8))
+    rms = float(torch.sqrt(torch.mean(r * r))) if r.numel() else 0.0
+    excess = (g - r).abs() - (ulp + RTOL_F32 * (r.abs() + rms))
+    bad = int((excess > 0).sum())
+    if bad:
+        i = int(torch.argmax(excess))
+        raise AssertionError(f"{what}: {bad} elements differ by more than one bf16 rounding step; worst at "
+                             f"{i}: got {float(g[i])!r} oracle {float(r[i])!r}")
+    nr = float(torch.linalg.vector_norm(r))
+    if nr > 0:
+        rel = float(torch.linalg.vector_norm(g - r)) / nr
+        assert rel <= BF16_REL_NORM, f"{what}: relative norm error {rel:.3e}"
+
+
 def assert_scalars(gpu, ref, what, rtol=RTOL_SCALAR):
     gpu = np.asarray(gpu, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
