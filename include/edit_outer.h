@@ -259,6 +259,35 @@ const char *edit_outer_strerror(edit_status_t s);
 /* Message of the last failure on the calling thread ("" if none). */
 const char *edit_outer_last_error(void);
 
+/* ---- a step that allocates nothing ------------------------------------ */
+
+/* Bytes of the fixed device array edit_outer_step_layer_noalloc works in. */
+#define EDIT_NOALLOC_SCRATCH_BYTES (1u << 20)
+
+/* For callers that cannot allocate device memory when they step (code under
+ * HIP graph capture, serving loops, harnesses that forbid hipMalloc): the
+ * step of edit_outer_step_layer, with the same kernels and the same results
+ * bit for bit, except that the per-block partial sums of its Gram pass live
+ * in a fixed array of EDIT_NOALLOC_SCRATCH_BYTES that the library keeps on
+ * each GPU for the life of the process (set up by edit_outer_init) instead
+ * of the handle's scratch memory.  The call allocates nothing: no hipMalloc,
+ * no hipFree, no event creation; kernel timing (edit_outer_set_profiling)
+ * does not apply to it.  The handle (made earlier, outside any capture)
+ * still holds the unit's EMA state and decision record.
+ * Arguments, ownership and errors as in edit_outer_step_layer, plus
+ * EDIT_EINVAL when the handle was made with EDIT_ONE_PASS, or when the
+ * unit's partials exceed the array: K(K+1)/2 doubles per Gram-pass block,
+ * whose count grows with the unit up to one block per CU above K = 8 (255
+ * on MI355X), so only K = 32 units of more than 63,488 16-byte vectors
+ * (507,904 bf16 or 253,952 fp32 elements) are refused there.
+ * All calls on one GPU share that GPU's array, which keeps the last call's
+ * partials (nothing in it needs clearing: a call writes every partial it
+ * reads).  Calls on one GPU must therefore not overlap: order them on one
+ * stream or with events, also across handles and host threads; overlapping
+ * calls race. */
+edit_status_t edit_outer_step_layer_noalloc(edit_outer_t h, int32_t layer, float *theta,
+                                            float *momentum, void *const *replicas, void *stream);
+
 /* ---- one worker of a sync group on its own GPU ------------------------- */
 
 /* In EDiT a module's K replicas belong to the K workers of a model sync

@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -79,6 +80,40 @@ struct Offload {
 
 }  // namespace
 
+// Device scratch of edit_outer_step_layer_noalloc: the per-block Gram partials
+// of one step, in a fixed array that each GPU holds for the life of the
+// process (no allocation per call).  Host code never names the array itself
+// (on the host `scratch` is only a stand-in for the symbol): its device
+// address comes from hipGetSymbolAddress, taken once per device at the first
+// edit_outer_init on that device, with that device current.
+constexpr size_t kNoAllocScratchBytes = size_t(1) << 20;  // EDIT_NOALLOC_SCRATCH_BYTES
+static_assert(kNoAllocScratchBytes == EDIT_NOALLOC_SCRATCH_BYTES, "header and library disagree");
+static __device__ __align__(256) double scratch[kNoAllocScratchBytes / sizeof(double)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};  // device address of `scratch` on each device
+
+// The device address of the scratch array on `device` (current), looked up
+// on first use.
+edit_status_t noalloc_scratch(int device, void** out) {
+  if (device < 0 || device >= kMaxDevices)
+    return fail(EDIT_EINVAL, "device index " + std::to_string(device) + " beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[device]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) return fail_hip(e, "hipGetSymbolAddress(scratch)");
+    g_scratch_ptr[device] = ptr;
+  }
+  *out = g_scratch_ptr[device];
+  return EDIT_OK;
+}
+
+}  // namespace
+
 struct edit_outer {
   edit_outer_config_t cfg{};
   std::vector<int64_t> numel;
@@ -87,6 +122,7 @@ struct edit_outer {
   int cap1 = 1;            // resident blocks of pass 1 on the whole GPU
   int32_t profile_every = 0;  // record kernel events on units l with l % every == 0
   char* arena = nullptr;   // one device allocation for every unit's scratch
+  void* noalloc = nullptr; // this device's fixed scratch array (step_layer_noalloc)
   FinishEntry* finish_table = nullptr;  // one-pass mode: [L] entries, in the arena
   bool one_pass = false;
   Offload off;
@@ -260,6 +296,8 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
   EDIT_TRY(validate_config(cfg));
   int dev = 0, num_cu = 0;
   EDIT_TRY(current_gfx950(&dev, &num_cu));
+  void* noalloc = nullptr;
+  EDIT_TRY(noalloc_scratch(dev, &noalloc));
   hipError_t e = hipSuccess;
 
   edit_outer* h = new (std::nothrow) edit_outer;
@@ -269,6 +307,7 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
   h->cfg.layer_numel = h->numel.data();
   h->device = dev;
   h->num_cu = num_cu;
+  h->noalloc = noalloc;
   const bool bf16 = cfg->replica_dtype == EDIT_BF16;
   h->cap1 = h->num_cu * pass1_blocks_per_cu(K, bf16);
   h->one_pass = (cfg->flags & EDIT_ONE_PASS) != 0;
@@ -582,6 +621,37 @@ edit_status_t edit_outer_step_layer(edit_outer_t h, int32_t layer, float* theta,
   EDIT_TRY(q.pass2(layer, theta, momentum, replicas));
   EDIT_TRY(q.event(h->units[layer], layer, 3));
   return q.finish(layer);
+}
+
+edit_status_t edit_outer_step_layer_noalloc(edit_outer_t h, int32_t layer, float* theta, float* momentum,
+                                            void* const* replicas, void* stream) {
+  if (!h) return fail(EDIT_EINVAL, "NULL handle");
+  if (h->one_pass) return fail(EDIT_EINVAL, "edit_outer_step_layer_noalloc is not available with EDIT_ONE_PASS");
+  EDIT_TRY(check_step(h, layer, theta, momentum, replicas));
+  const int K = h->cfg.num_workers;
+  Unit& u = h->units[layer];
+  const size_t need = static_cast<size_t>(num_pairs(K)) * static_cast<size_t>(u.rows) * sizeof(double);
+  if (need > kNoAllocScratchBytes)
+    return fail(EDIT_EINVAL, "unit " + std::to_string(layer) + " needs " + std::to_string(need) +
+                                 " bytes of partial sums; the fixed scratch holds " +
+                                 std::to_string(kNoAllocScratchBytes));
+  EDIT_TRY(check_device(h));
+  const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const bool bf16 = h->cfg.replica_dtype == EDIT_BF16;
+  const DecideParams prm = decide_params(h);
+  double* partials = static_cast<double*>(h->noalloc);  // the device address, never `scratch` itself
+  const void* const* creps = u.n == 0 ? kNoReplicas : const_cast<const void* const*>(replicas);
+  hipError_t e = launch_pass1(K, bf16, u.rows, theta, creps, u.n, partials, nullptr, 0, nullptr, prm, s);
+  if (e != hipSuccess) return fail_hip(e, "pass1 launch");
+  if ((e = launch_decide(K, partials, u.rows, u.rec, prm, s)) != hipSuccess) return fail_hip(e, "decide launch");
+  Enqueue q{h, s, prm, K, bf16};
+  EDIT_TRY(q.pass2(layer, theta, momentum, replicas));
+  if ((e = hipEventRecord(u.done, s)) != hipSuccess) return fail_hip(e, "hipEventRecord");
+  u.pending = true;
+  u.done_slot = -1;
+  u.profiled = false;
+  u.has_state = true;
+  return EDIT_OK;
 }
 
 edit_status_t edit_outer_gram_layer(edit_outer_t h, int32_t layer, const float* theta,

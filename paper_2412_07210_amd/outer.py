@@ -28,7 +28,7 @@ EDIT_OK, EDIT_EINVAL, EDIT_ENOMEM, EDIT_EHIP, EDIT_ESTATE, EDIT_ENODEV = 0, -1, 
 
 # Every function the header declares; the CPU tests check the library exports them.
 EXPORTS = (
-    "edit_outer_init", "edit_outer_min_warmup", "edit_outer_step_layer",
+    "edit_outer_init", "edit_outer_min_warmup", "edit_outer_step_layer", "edit_outer_step_layer_noalloc",
     "edit_outer_step_round",
     "edit_outer_step_round_host", "edit_outer_gram_layer", "edit_outer_apply_layer",
     "edit_outer_state_get", "edit_outer_state_set",
@@ -99,6 +99,8 @@ def load_library() -> ctypes.CDLL:
     lib.edit_outer_min_warmup.restype = ctypes.c_int64
     lib.edit_outer_step_layer.argtypes = [vp, ctypes.c_int32, vp, vp, ctypes.POINTER(vp), vp]
     lib.edit_outer_step_layer.restype = st
+    lib.edit_outer_step_layer_noalloc.argtypes = [vp, ctypes.c_int32, vp, vp, ctypes.POINTER(vp), vp]
+    lib.edit_outer_step_layer_noalloc.restype = st
     lib.edit_outer_step_round.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
                                           ctypes.POINTER(vp), ctypes.POINTER(vp),
                                           ctypes.POINTER(vp), vp]
