@@ -346,9 +346,11 @@ def _profile_cmds(variant: str) -> dict:
         "trace": f"rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace{sfx} -o {tag} -- "
                  f"python bench.py{flag}",
         "fetch": f"rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/prof_fetch{sfx} -o {tag} -- "
-                 f"python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0{flag}",
+                 f"python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0 --secondary 0 "
+                 f"--update-probe 0{flag}",
         "write": f"rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/prof_write{sfx} -o {tag} -- "
-                 f"python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0{flag}",
+                 f"python bench.py --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0 --secondary 0 "
+                 f"--update-probe 0{flag}",
     }
 
 
@@ -360,7 +362,8 @@ PASS1_KINDS = ("pass1_gram_kernel", "pass1_gram_mfma_kernel", PAIR2, PAIR1)
 UNITS_PER_LAUNCH = {PAIR2: 2}
 
 SHORT = {"pass1_gram_kernel": "pass1", PAIR2: "pass1_pair", PAIR1: "pass1_pair1", "decide_kernel": "decide",
-         "pass2_update_kernel": "pass2", "fused_mean_kernel": "fused", "fused_finish_kernel": "finish"}
+         "pass2_update_kernel": "pass2", "fused_mean_kernel": "fused", "fused_finish_kernel": "finish",
+         "update_pattern_probe_kernel": "probe"}
 
 
 def _kernel_kind(name: str) -> str:
@@ -368,7 +371,8 @@ def _kernel_kind(name: str) -> str:
     if m:
         return PAIR2 if m.group(1) == "2" else PAIR1
     for kind in ("pass1_gram_kernel", "pass1_gram_mfma_kernel", "decide_kernel", "pass2_update_kernel",
-                 "round_small_kernel", "fused_mean_kernel", "fused_finish_kernel", "copy_kernel"):
+                 "round_small_kernel", "fused_mean_kernel", "fused_finish_kernel", "update_pattern_probe_kernel",
+                 "copy_kernel"):
         if kind in name:
             return kind
     return ""
@@ -472,12 +476,13 @@ def summarize_profiles(out_dir: str, bench_json: str, variant: str = "two-pass")
     tag, sfx = cmds["tag"], cmds["suffix"]
     one = variant == "one-pass"
     kinds = ("fused_mean_kernel", "fused_finish_kernel") if one else \
-        ("pass1_gram_kernel", PAIR2, PAIR1, "decide_kernel", "pass2_update_kernel")
+        ("pass1_gram_kernel", PAIR2, PAIR1, "decide_kernel", "pass2_update_kernel", "update_pattern_probe_kernel")
     dominant = "fused_mean_kernel" if one else "pass2_update_kernel"
     wl = synth.get(DEFAULT_WORKLOAD)
     n, K, R = wl.layer_numel[0], wl.num_workers, wl.replica_bytes
     algo = {"pass1_gram_kernel": n * (4 + K * R), PAIR2: 2 * n * (4 + K * R), PAIR1: n * (4 + K * R),
             "pass2_update_kernel": n * (8 + K * R + 8 + K * R),
+            "update_pattern_probe_kernel": n * (8 + K * R + 8 + K * R),
             "fused_mean_kernel": n * (8 + K * R + 8 + K * R)}
     title = "one-pass mean step (no penalty components)" if one else "outer step"
     prof_dir = os.path.join(ROOT, "profiles")
@@ -486,16 +491,30 @@ def summarize_profiles(out_dir: str, bench_json: str, variant: str = "two-pass")
     with open(bench_json) as f:
         bench = json.load(f)
 
-    # kernel trace statistics
-    stats = {}
-    with open(os.path.join(out_dir, f"prof_trace{sfx}", f"{tag}_kernel_stats.csv")) as f:
+    # kernel durations of the headline workload: the default run also steps
+    # the secondary workloads afterwards, the first of them with fp32
+    # replicas, so the headline's dispatches are those before the first
+    # method kernel built for fp32 replicas (template argument false)
+    disp = []
+    with open(os.path.join(out_dir, f"prof_trace{sfx}", f"{tag}_kernel_trace.csv")) as f:
         for row in csv.DictReader(f):
-            kind = _kernel_kind(row["Name"])
-            if kind:
-                stats[kind] = {k: float(row[k]) for k in ("Calls", "AverageNs", "MinNs", "MaxNs")}
+            kind = _kernel_kind(row["Kernel_Name"])
+            if kind and kind != "copy_kernel":
+                disp.append((int(row["Start_Timestamp"]), int(row["End_Timestamp"]), kind,
+                             bool(re.search(r"ILi\d+ELb0E", row["Kernel_Name"]))))
+    disp.sort()
+    cutoff = next((t0 for t0, _, _, f32 in disp if f32), None)
+    durs = {}
+    for t0, t1, kind, _ in disp:
+        if cutoff is None or t0 < cutoff:
+            durs.setdefault(kind, []).append(t1 - t0)
+    stats = {k: {"Calls": len(v), "AverageNs": sum(v) / len(v), "MinNs": min(v), "MaxNs": max(v)}
+             for k, v in durs.items()}
     lines = [f"# Kernel durations: 1B K=8 {title} (24 units x 51,384,320, bf16 replicas)", "",
              "Command (from the repository root; `<out>` = the directory the profiler wrote to):", "",
              "    " + cmds["trace"], "",
+             "Dispatches of the headline workload only (those before the secondary workloads' first "
+             "kernel); summarised with `python bench.py --summarize-profiles <out> <bench json>`.", "",
              "| kernel | calls | avg us | min us | max us | algorithmic bytes | GB/s at avg |",
              "|---|---|---|---|---|---|---|"]
     for kind in kinds:
@@ -739,6 +758,53 @@ def summarize_group_trace(out_dir: str, bench_json: str) -> str:
     return text
 
 
+# SQ counters of the matrix-core Gram pass, two rocprofv3 --pmc runs (at most
+# eight SQ counters each) of a short K = 16 run.
+SQ_PASSES = {
+    "a": ["SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_INST_ANY",
+          "SQ_WAVE_CYCLES", "SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU_CVT", "GRBM_GUI_ACTIVE"],
+    "b": ["SQ_INSTS_VALU_ADD_F64", "SQ_INSTS_VALU_MFMA_F64", "SQ_INSTS_VALU_MFMA_MOPS_F64", "SQ_INSTS_VALU_INT32",
+          "SQ_INSTS_VALU_FMA_F64", "SQ_WAIT_ANY", "SQ_INSTS_SALU", "SQ_ACTIVE_INST_ANY"],
+}
+SQ_WORKLOAD_ARGS = ("--config aedit1b-k16-bf16 --units 3 --steps 2 --warmup 1 --no-cpu-baseline --profile-every 0 "
+                    "--secondary 0 --update-probe 0 --no-copy-probe --no-settle")
+
+
+def sq_commands() -> dict:
+    return {k: f"rocprofv3 --pmc {' '.join(v)} -f csv -d <out>/prof_sq_{k} -o sq -- python bench.py "
+               f"{SQ_WORKLOAD_ARGS}" for k, v in SQ_PASSES.items()}
+
+
+def summarize_sq_counters(out_dir: str) -> str:
+    """profiles/ table of the Gram pass's SQ counters (K = 16, one
+    51,380,224-element unit per dispatch): per-dispatch averages and what
+    they say about the pass's bound."""
+    import csv
+
+    vals = {}
+    for k in SQ_PASSES:
+        with open(os.path.join(out_dir, f"prof_sq_{k}", "sq_counter_collection.csv")) as f:
+            for row in csv.DictReader(f):
+                if "pass1_gram_mfma_kernel" not in row["Kernel_Name"] or int(row["Grid_Size"]) < 100_000:
+                    continue  # the unit's launches, not the gains' single blocks
+                vals.setdefault(row["Counter_Name"], []).append(float(row["Counter_Value"]))
+    avg = {c: sum(v) / len(v) for c, v in vals.items()}
+    n = 51_380_224
+    lines = ["# SQ counters of the matrix-core Gram pass: K = 16, bf16, 51,380,224-element unit", "",
+             "Commands (from the repository root; `<out>` = the directory the profiler wrote to):", ""]
+    lines += ["    " + c for c in sq_commands().values()]
+    lines += ["", f"Summarised with `python bench.py --summarize-sq-counters <out>`; per-dispatch averages over "
+              f"{min(len(v) for v in vals.values())} dispatches of pass1_gram_mfma_kernel on the unit.", "",
+              "| counter | per dispatch | per element |", "|---|---|---|"]
+    for c in SQ_PASSES["a"] + SQ_PASSES["b"]:
+        if c in avg:
+            lines.append(f"| {c} | {avg[c]:.4g} | {avg[c] / n:.4g} |")
+    text = "\n".join(lines) + "\n"
+    with open(os.path.join(ROOT, "profiles", "aedit1b_k16_gram_pass_sq_counters.md"), "w") as f:
+        f.write(text)
+    return text
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[1])
     ap.add_argument("--gpus", type=int, default=1)
@@ -784,11 +850,16 @@ def main(argv=None) -> int:
                     help="which step --summarize-profiles reads (default: the two-pass step)")
     ap.add_argument("--summarize-group-trace", nargs=2, metavar=("OUT_DIR", "BENCH_JSON"),
                     help="write the profiles/ table of a traced --sync-group-rank run (no GPU)")
+    ap.add_argument("--summarize-sq-counters", metavar="OUT_DIR",
+                    help="write the profiles/ table of the K = 16 Gram pass's SQ counters (no GPU)")
     ap.add_argument("--summarize-trace", nargs=2, metavar=("OUT_DIR", "WORKLOAD"),
                     help="write a per-unit-size kernel table from a rocprofv3 kernel trace (no GPU)")
     args = ap.parse_args(argv)
     if args.summarize_profiles:
         summarize_profiles(*args.summarize_profiles, variant=args.profile_variant)
+        return 0
+    if args.summarize_sq_counters:
+        print(summarize_sq_counters(args.summarize_sq_counters))
         return 0
     if args.summarize_trace:
         print(summarize_trace_by_grid(*args.summarize_trace))

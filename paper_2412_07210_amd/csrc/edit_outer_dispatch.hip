@@ -56,10 +56,23 @@ hipError_t launch_decide_gram(int K, const double* gram, UnitRecord* rec, const 
   return s ? s->decide_gram(gram, rec, prm, stream) : hipErrorInvalidValue;
 }
 
-hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom, void* const* reps,
+hipError_t launch_pass2(int K, bool bf16, int blocks, int lds, float* theta, float* mom, void* const* reps,
                         const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
   const KernelSet* s = kernels_for(K);
-  return s ? s->pass2(bf16, blocks, theta, mom, reps, rec, n, lr, rho, stream) : hipErrorInvalidValue;
+  return s ? s->pass2(bf16, blocks, lds, theta, mom, reps, rec, n, lr, rho, stream) : hipErrorInvalidValue;
+}
+
+// The update pass streams 2K + 4 buffers at once (K + 2 read, K + 2
+// written).  With fewer of its waves resident per CU the HBM serves that
+// mix faster: at the 1B shape (K = 8, bf16) 410-421 us per unit at three
+// 128-thread blocks per CU (6 waves) against 442-444 us at the eight its
+// registers allow, and 1.5-3.6% shorter rounds at every K = 8 workload;
+// above K = 8 four blocks (8 waves) measured best (A/B runs on one box).
+int update_pass_blocks_per_cu(int K) { return K <= 8 ? 3 : 4; }
+
+int update_pass_lds(int K, int lds_per_cu) {
+  // the largest multiple of 256 bytes that still lets that many blocks fit
+  return lds_per_cu > 0 ? (lds_per_cu / update_pass_blocks_per_cu(K)) & ~255 : 0;
 }
 
 int fused_vectors_per_thread(int K, bool bf16) {
@@ -80,10 +93,10 @@ hipError_t launch_fused_finish(int K, const FinishEntry* table, int units, hipSt
   return s ? s->fused_finish(table, units, stream) : hipErrorInvalidValue;
 }
 
-hipError_t launch_pattern_probe(int K, bool bf16, int blocks, float* theta, float* mom, void* const* reps,
+hipError_t launch_pattern_probe(int K, bool bf16, int blocks, int lds, float* theta, float* mom, void* const* reps,
                                 int64_t n, hipStream_t stream) {
   const KernelSet* s = kernels_for(K);
-  return s ? s->pattern_probe(bf16, blocks, theta, mom, reps, n, stream) : hipErrorInvalidValue;
+  return s ? s->pattern_probe(bf16, blocks, lds, theta, mom, reps, n, stream) : hipErrorInvalidValue;
 }
 
 int pass1_blocks_per_cu(int K, bool bf16) {

@@ -98,14 +98,14 @@ struct KernelSet {
                        hipStream_t stream);
   hipError_t (*gram_reduce)(const double* partials, int rows, double* gram, hipStream_t stream);
   hipError_t (*decide_gram)(const double* gram, UnitRecord* rec, const DecideParams& prm, hipStream_t stream);
-  hipError_t (*pass2)(bool bf16, int blocks, float* theta, float* mom, void* const* reps, const UnitRecord* rec,
-                      int64_t n, double lr, double rho, hipStream_t stream);
+  hipError_t (*pass2)(bool bf16, int blocks, int lds, float* theta, float* mom, void* const* reps,
+                      const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream);
   hipError_t (*fused_mean)(bool bf16, int rows, float* theta, float* mom, void* const* reps, double* partials,
                            UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream);
   hipError_t (*fused_finish)(const FinishEntry* table, int units, hipStream_t stream);
   int (*pass1_blocks_per_cu)(bool bf16);
-  hipError_t (*pattern_probe)(bool bf16, int blocks, float* theta, float* mom, void* const* reps, int64_t n,
-                              hipStream_t stream);
+  hipError_t (*pattern_probe)(bool bf16, int blocks, int lds, float* theta, float* mom, void* const* reps,
+                              int64_t n, hipStream_t stream);
   int fused_vectors_bf16, fused_vectors_f32;
 };
 
@@ -141,9 +141,15 @@ hipError_t launch_gram_reduce(int K, const double* partials, int rows, double* g
 // The decision from a device-resident Gram vector.
 hipError_t launch_decide_gram(int K, const double* gram, UnitRecord* rec, const DecideParams& prm,
                               hipStream_t stream);
-hipError_t launch_pass2(int K, bool bf16, int blocks, float* theta, float* mom,
+// The update pass; `lds` bytes of dynamic LDS per block (used by nothing)
+// cap its resident blocks per CU (update_pass_lds).
+hipError_t launch_pass2(int K, bool bf16, int blocks, int lds, float* theta, float* mom,
                         void* const* reps, const UnitRecord* rec, int64_t n, double lr,
                         double rho, hipStream_t stream);
+// Update-pass blocks resident per CU, and the dynamic LDS per block that
+// caps them there given the CU's LDS bytes.
+int update_pass_blocks_per_cu(int K);
+int update_pass_lds(int K, int lds_per_cu);
 // One-pass mean step (no penalty components): `rows` blocks of
 // fused_vectors_per_thread(K, bf16) * kFusedThreads vectors each, leaving
 // (K+1) x rows norm partials and the unit marked; then one block per entry
@@ -156,7 +162,7 @@ hipError_t launch_fused_finish(int K, const FinishEntry* table, int units, hipSt
 hipError_t launch_copy(void* dst, const void* src, int64_t nbytes, int blocks,
                        hipStream_t stream);
 // Pass 2's loads and stores (whole vectors only) with no arithmetic.
-hipError_t launch_pattern_probe(int K, bool bf16, int blocks, float* theta, float* mom, void* const* reps,
+hipError_t launch_pattern_probe(int K, bool bf16, int blocks, int lds, float* theta, float* mom, void* const* reps,
                                 int64_t n, hipStream_t stream);
 
 // Resident blocks per CU of the pass-1 kernel (for its persistent grid).

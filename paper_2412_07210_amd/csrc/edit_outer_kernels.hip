@@ -513,6 +513,16 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_pair_kernel(Pas
 // Vector slots per lane per loop trip of the matrix-core pass (two, or
 // loads two trips ahead, measured no faster and need 512-thread blocks).
 constexpr int kMfmaSlots = 1;
+// Load buffers per lane in the matrix-core pass's loop: two (the next trip's
+// loads in flight while one is computed).  Three, four or six buffers at
+// K = 16 (111-165 VGPRs, no spills, up to 3x the bytes in flight) measured
+// the same round time (A/B on one box), so the pass is not waiting on
+// memory latency: its matrix-core and vector instructions share one issue
+// port and take its time.
+template <int K>
+constexpr int kMfmaDepth() {
+  return 2;
+}
 
 template <int K>
 struct Tiles4 {
@@ -618,6 +628,7 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_mfma_kernel(con
   }
   const int b = static_cast<int>(blockIdx.x) - first;  // this block's partial row
   const int rows = static_cast<int>(gridDim.x) - first;
+  constexpr int kDepth = kMfmaDepth<K>();
 #include "gram_rows_mfma.inc"
 }
 // ---------------------------------------------------------------- decide
@@ -817,6 +828,7 @@ __device__ void single_block_unit(const SingleBlockUnit<K>& su, const DecidePara
     double* __restrict__ partials = su.partials;
     const int b = 0, rows = 1;
     if constexpr (MFMA) {
+      constexpr int kDepth = 2;  // a few trips at most: deeper prefetch only costs registers
 #include "gram_rows_mfma.inc"
     } else {
       constexpr int NP = K * (K + 1) / 2;
@@ -1170,24 +1182,24 @@ hipError_t decide_gram_launch(const double* gram, UnitRecord* rec, const DecideP
 }
 
 template <int K, bool BF16>
-hipError_t pattern_probe_launch(int blocks, float* theta, float* mom, void* const* reps, int64_t n,
+hipError_t pattern_probe_launch(int blocks, int lds, float* theta, float* mom, void* const* reps, int64_t n,
                                 hipStream_t stream) {
   MutPtrs<K> rp;
   for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
   const int64_t nvec = n / Vec<BF16>::VE;
-  hipLaunchKernelGGL((update_pattern_probe_kernel<K, BF16, kNT2>), dim3(blocks), dim3(kPass2Threads), 0, stream,
+  hipLaunchKernelGGL((update_pattern_probe_kernel<K, BF16, kNT2>), dim3(blocks), dim3(kPass2Threads), lds, stream,
                      theta, mom, rp, nvec, 0u);
   return hipGetLastError();
 }
 
 template <int K, bool BF16>
-hipError_t pass2_launch(int blocks, float* theta, float* mom, void* const* reps,
+hipError_t pass2_launch(int blocks, int lds, float* theta, float* mom, void* const* reps,
                         const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
   MutPtrs<K> rp;
   for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
   const int64_t nvec = n / Vec<BF16>::VE;
-  hipLaunchKernelGGL((pass2_update_kernel<K, BF16, kNT2>), dim3(blocks), dim3(kPass2Threads), 0, stream,
-                     theta, mom, rp, rec, nvec, n, lr, rho);
+  hipLaunchKernelGGL((pass2_update_kernel<K, BF16, kNT2>), dim3(blocks), dim3(kPass2Threads), lds, stream, theta,
+                     mom, rp, rec, nvec, n, lr, rho);
   return hipGetLastError();
 }
 
@@ -1246,15 +1258,15 @@ struct Launchers {
     return bf16 ? round_small_launch<K, true>(prev, nprev, prm, unit, count, lr, rho, stream)
                 : round_small_launch<K, false>(prev, nprev, prm, unit, count, lr, rho, stream);
   }
-  static hipError_t pass2(bool bf16, int blocks, float* theta, float* mom, void* const* reps,
+  static hipError_t pass2(bool bf16, int blocks, int lds, float* theta, float* mom, void* const* reps,
                           const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
-    return bf16 ? pass2_launch<K, true>(blocks, theta, mom, reps, rec, n, lr, rho, stream)
-                : pass2_launch<K, false>(blocks, theta, mom, reps, rec, n, lr, rho, stream);
+    return bf16 ? pass2_launch<K, true>(blocks, lds, theta, mom, reps, rec, n, lr, rho, stream)
+                : pass2_launch<K, false>(blocks, lds, theta, mom, reps, rec, n, lr, rho, stream);
   }
-  static hipError_t pattern_probe(bool bf16, int blocks, float* theta, float* mom, void* const* reps, int64_t n,
-                                  hipStream_t stream) {
-    return bf16 ? pattern_probe_launch<K, true>(blocks, theta, mom, reps, n, stream)
-                : pattern_probe_launch<K, false>(blocks, theta, mom, reps, n, stream);
+  static hipError_t pattern_probe(bool bf16, int blocks, int lds, float* theta, float* mom, void* const* reps,
+                                  int64_t n, hipStream_t stream) {
+    return bf16 ? pattern_probe_launch<K, true>(blocks, lds, theta, mom, reps, n, stream)
+                : pattern_probe_launch<K, false>(blocks, lds, theta, mom, reps, n, stream);
   }
   static hipError_t fused_mean(bool bf16, int rows, float* theta, float* mom, void* const* reps,
                                double* partials, UnitRecord* rec, int64_t n, double lr, double rho,

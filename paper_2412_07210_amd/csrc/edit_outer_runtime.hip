@@ -119,6 +119,7 @@ struct edit_outer {
   std::vector<int64_t> numel;
   int device = 0;
   int num_cu = 0;
+  int pass2_lds = 0;       // dynamic LDS per update-pass block (occupancy cap)
   int cap1 = 1;            // resident blocks of pass 1 on the whole GPU
   int32_t profile_every = 0;  // record kernel events on units l with l % every == 0
   char* arena = nullptr;   // one device allocation for every unit's scratch
@@ -307,6 +308,15 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
   h->cfg.layer_numel = h->numel.data();
   h->device = dev;
   h->num_cu = num_cu;
+  {
+    int lds_per_cu = 0;
+    e = hipDeviceGetAttribute(&lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev);
+    if (e != hipSuccess) {
+      delete h;
+      return fail_hip(e, "hipDeviceGetAttribute(LDS per CU)");
+    }
+    h->pass2_lds = update_pass_lds(K, lds_per_cu);
+  }
   h->noalloc = noalloc;
   const bool bf16 = cfg->replica_dtype == EDIT_BF16;
   h->cap1 = h->num_cu * pass1_blocks_per_cu(K, bf16);
@@ -522,7 +532,7 @@ struct Enqueue {
   edit_status_t pass2(int32_t layer, float* theta, float* momentum, void* const* replicas) {
     Unit& u = h->units[layer];
     void* const* mreps = u.n == 0 ? kNoReplicas : replicas;
-    hipError_t e = launch_pass2(K, bf16, u.blocks2, theta, momentum, mreps, u.rec, u.n,
+    hipError_t e = launch_pass2(K, bf16, u.blocks2, h->pass2_lds, theta, momentum, mreps, u.rec, u.n,
                                 h->cfg.outer_lr, h->cfg.momentum, s);
     if (e != hipSuccess) return fail_hip(e, "pass2 launch");
     return EDIT_OK;
@@ -1053,8 +1063,9 @@ edit_status_t edit_outer_update_probe(edit_outer_t h, int32_t layer, float* thet
   EDIT_TRY(check_device(h));
   const Unit& u = h->units[layer];
   if (u.n == 0) return EDIT_OK;
-  const hipError_t e = launch_pattern_probe(h->cfg.num_workers, h->cfg.replica_dtype == EDIT_BF16, u.blocks2, theta,
-                                            momentum, replicas, u.n, reinterpret_cast<hipStream_t>(stream));
+  const hipError_t e =
+      launch_pattern_probe(h->cfg.num_workers, h->cfg.replica_dtype == EDIT_BF16, u.blocks2, h->pass2_lds, theta,
+                           momentum, replicas, u.n, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? EDIT_OK : fail_hip(e, "update probe launch");
 }
 
