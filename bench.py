@@ -408,7 +408,7 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
     def unit_of(kind, grid):
         for n in sizes:
             nvec = -(-n // ve)
-            if kind == "pass2_update_kernel" and -(-nvec // 128) * 128 == grid:
+            if kind in ("pass2_update_kernel", "update_pattern_probe_kernel") and -(-nvec // 128) * 128 == grid:
                 return n
             tpb = 768 if kind == "pass1_gram_mfma_kernel" else 256  # threads per Gram-pass block
             if kind in PASS1_KINDS and -(-nvec // 256) >= grid // tpb - 1:
@@ -420,11 +420,13 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
     def algo(kind, n):
         if kind in PASS1_KINDS:
             return UNITS_PER_LAUNCH.get(kind, 1) * n * (4 + K * R)
+        if kind == "update_pattern_probe_kernel":  # every replica, whole vectors only
+            return (n // (16 // R)) * (16 // R) * (16 + 2 * K * R)
         return n * (16 + 2 * K * R) if kind == "pass2_update_kernel" else None
     lines = [f"# Kernel durations by unit size: {wl.description}", "",
              "Command (from the repository root; `<out>` = the directory the profiler wrote to):", "",
              f"    rocprofv3 --kernel-trace --stats -f csv -d <out>/prof_trace_{tag} -o {tag} -- "
-             f"python bench.py --config {name} --steps 10 --warmup 5 --no-cpu-baseline", "",
+             f"python bench.py --config {name} --steps 10 --warmup 5 --no-cpu-baseline --secondary 0", "",
              f"Summarised with `python bench.py --summarize-trace <out> {name}` (groups the trace's "
              "dispatches by kernel and grid size).", "",
              "| kernel | grid work-items | unit elements | calls | avg us | min us | max us | "
@@ -501,7 +503,7 @@ def summarize_profiles(out_dir: str, bench_json: str, variant: str = "two-pass")
             kind = _kernel_kind(row["Kernel_Name"])
             if kind and kind != "copy_kernel":
                 disp.append((int(row["Start_Timestamp"]), int(row["End_Timestamp"]), kind,
-                             bool(re.search(r"ILi\d+ELb0E", row["Kernel_Name"]))))
+                             bool(re.search(r"<\d+, false|ILi\d+ELb0E", row["Kernel_Name"]))))
     disp.sort()
     cutoff = next((t0 for t0, _, _, f32 in disp if f32), None)
     durs = {}
