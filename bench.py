@@ -408,7 +408,7 @@ def summarize_trace_by_grid(out_dir: str, name: str) -> str:
     def unit_of(kind, grid):
         for n in sizes:
             nvec = -(-n // ve)
-            if kind in ("pass2_update_kernel", "update_pattern_probe_kernel") and -(-nvec // 128) * 128 == grid:
+            if kind in ("pass2_update_kernel", "update_pattern_probe_kernel") and -(-nvec // 64) * 64 == grid:
                 return n
             tpb = 768 if kind == "pass1_gram_mfma_kernel" else 256  # threads per Gram-pass block
             if kind in PASS1_KINDS and -(-nvec // 256) >= grid // tpb - 1:

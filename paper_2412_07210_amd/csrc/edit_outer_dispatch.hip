@@ -63,12 +63,17 @@ hipError_t launch_pass2(int K, bool bf16, int blocks, int lds, float* theta, flo
 }
 
 // The update pass streams 2K + 4 buffers at once (K + 2 read, K + 2
-// written).  With fewer of its waves resident per CU the HBM serves that
-// mix faster: at the 1B shape (K = 8, bf16) 410-421 us per unit at three
-// 128-thread blocks per CU (6 waves) against 442-444 us at the eight its
-// registers allow, and 1.5-3.6% shorter rounds at every K = 8 workload;
-// above K = 8 four blocks (8 waves) measured best (A/B runs on one box).
-int update_pass_blocks_per_cu(int K) { return K <= 8 ? 3 : 4; }
+// written), and the HBM serves that mix faster with fewer of its waves in
+// flight than its registers allow.  Sweeps on one box (alternating runs,
+// 1B round at K = 8 bf16): 128-thread blocks, 8 per CU (the register
+// limit) 14.31-14.36 ms, 4 per CU 13.91-14.01, 3 per CU 13.84-13.87;
+// one-wave blocks, 6 per CU 13.56-13.60 ms, against 13.60-13.68 at 4 or 5,
+// 13.72-13.73 at 7 and 14.00-14.02 at 8.  Six one-wave blocks per CU also
+// gave the shortest 350M, 7B half-shard and A-EDiT K = 16 rounds.
+int update_pass_blocks_per_cu(int K) {
+  (void)K;
+  return 6;
+}
 
 int update_pass_lds(int K, int lds_per_cu) {
   // the largest multiple of 256 bytes that still lets that many blocks fit
@@ -80,11 +85,22 @@ int fused_vectors_per_thread(int K, bool bf16) {
   return s ? (bf16 ? s->fused_vectors_bf16 : s->fused_vectors_f32) : 1;
 }
 
-hipError_t launch_fused_mean(int K, bool bf16, int rows, float* theta, float* mom, void* const* reps,
+// The one-pass kernel streams the same 2K + 4 buffers as the update pass.
+// With bf16 replicas (two 16-byte vectors per thread, 3 waves per SIMD by
+// its registers) four resident blocks per CU measured best at the 1B shape:
+// 10.64-10.73 ms per round against 11.02-11.07 ms uncapped, 10.86-10.93 at
+// three blocks and 15.4 at two (A/B runs on one box).  Other cases keep the
+// occupancy their registers give.
+int one_pass_lds(int K, bool bf16, int lds_per_cu) {
+  const int blocks = bf16 && K <= 16 ? 4 : 0;
+  return blocks > 0 && lds_per_cu > 0 ? (lds_per_cu / blocks) & ~255 : 0;
+}
+
+hipError_t launch_fused_mean(int K, bool bf16, int rows, int lds, float* theta, float* mom, void* const* reps,
                              double* partials, UnitRecord* rec, int64_t n, double lr, double rho,
                              hipStream_t stream) {
   const KernelSet* s = kernels_for(K);
-  return s ? s->fused_mean(bf16, rows, theta, mom, reps, partials, rec, n, lr, rho, stream)
+  return s ? s->fused_mean(bf16, rows, lds, theta, mom, reps, partials, rec, n, lr, rho, stream)
            : hipErrorInvalidValue;
 }
 

@@ -10,7 +10,7 @@
 namespace edit {
 
 constexpr int kThreads = 256;        // threads per block of the Gram pass
-constexpr int kPass2Threads = 128;   // threads per block of the update pass
+constexpr int kPass2Threads = 64;    // threads per block of the update pass (one wave)
 constexpr int kFusedThreads = 128;   // threads per block of the one-pass mean step
 constexpr int kMaxK = EDIT_MAX_K;
 constexpr int kMaxPairs = kMaxK * (kMaxK + 1) / 2;
@@ -100,8 +100,8 @@ struct KernelSet {
   hipError_t (*decide_gram)(const double* gram, UnitRecord* rec, const DecideParams& prm, hipStream_t stream);
   hipError_t (*pass2)(bool bf16, int blocks, int lds, float* theta, float* mom, void* const* reps,
                       const UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream);
-  hipError_t (*fused_mean)(bool bf16, int rows, float* theta, float* mom, void* const* reps, double* partials,
-                           UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream);
+  hipError_t (*fused_mean)(bool bf16, int rows, int lds, float* theta, float* mom, void* const* reps,
+                           double* partials, UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream);
   hipError_t (*fused_finish)(const FinishEntry* table, int units, hipStream_t stream);
   int (*pass1_blocks_per_cu)(bool bf16);
   hipError_t (*pattern_probe)(bool bf16, int blocks, int lds, float* theta, float* mom, void* const* reps,
@@ -155,7 +155,10 @@ int update_pass_lds(int K, int lds_per_cu);
 // (K+1) x rows norm partials and the unit marked; then one block per entry
 // of `table` turns marked units' partials into their records.
 int fused_vectors_per_thread(int K, bool bf16);
-hipError_t launch_fused_mean(int K, bool bf16, int rows, float* theta, float* mom,
+// `lds`: dynamic LDS per block capping its resident blocks per CU
+// (one_pass_lds), as for the update pass.
+int one_pass_lds(int K, bool bf16, int lds_per_cu);
+hipError_t launch_fused_mean(int K, bool bf16, int rows, int lds, float* theta, float* mom,
                              void* const* reps, double* partials, UnitRecord* rec, int64_t n,
                              double lr, double rho, hipStream_t stream);
 hipError_t launch_fused_finish(int K, const FinishEntry* table, int units, hipStream_t stream);

@@ -728,11 +728,13 @@ __device__ __forceinline__ void update_vector(float* theta, float* mom, const Mu
   for (int j = 0; j < K; ++j) st16<NT>(reinterpret_cast<u32x4*>(reps.p[j]) + v, out);
 }
 
-// One 16-byte vector of every buffer per thread, one block per 128 vectors
-// (a flat grid): the hardware dispatcher then keeps the in-flight window of
-// each of the 2K+4 streams short and ordered (measured 5.5 TB/s here against
-// 4.9 TB/s for a persistent grid-stride loop; 128-thread blocks edged out
-// 256).  Blocks are taken from the unit's end; forward order measured the
+// One 16-byte vector of every buffer per thread, one one-wave block per 64
+// vectors (a flat grid): the hardware dispatcher then keeps the in-flight
+// window of each of the 2K+4 streams short and ordered (measured 5.5 TB/s
+// here against 4.9 TB/s for a persistent grid-stride loop).  The launch
+// reserves dynamic LDS so that six blocks at most run on a CU
+// (update_pass_blocks_per_cu): fewer waves in flight serve this traffic
+// faster.  Blocks are taken from the unit's end; forward order measured the
 // same.
 template <int K, bool BF16, bool NT>
 __global__ __launch_bounds__(kPass2Threads) void pass2_update_kernel(float* __restrict__ theta,
@@ -1212,13 +1214,13 @@ constexpr int fused_v() {
 }
 
 template <int K, bool BF16>
-hipError_t fused_mean_launch(int rows, float* theta, float* mom, void* const* reps, double* partials,
+hipError_t fused_mean_launch(int rows, int lds, float* theta, float* mom, void* const* reps, double* partials,
                              UnitRecord* rec, int64_t n, double lr, double rho, hipStream_t stream) {
   MutPtrs<K> rp;
   for (int j = 0; j < K; ++j) rp.p[j] = reps[j];
   const int64_t nvec = n / Vec<BF16>::VE;
   hipLaunchKernelGGL((fused_mean_kernel<K, BF16, kNT2, fused_v<K, BF16>()>), dim3(rows), dim3(kFusedThreads),
-                     0, stream, theta, mom, rp, partials, rec, nvec, n, lr, rho);
+                     lds, stream, theta, mom, rp, partials, rec, nvec, n, lr, rho);
   return hipGetLastError();
 }
 
@@ -1268,11 +1270,11 @@ struct Launchers {
     return bf16 ? pattern_probe_launch<K, true>(blocks, lds, theta, mom, reps, n, stream)
                 : pattern_probe_launch<K, false>(blocks, lds, theta, mom, reps, n, stream);
   }
-  static hipError_t fused_mean(bool bf16, int rows, float* theta, float* mom, void* const* reps,
+  static hipError_t fused_mean(bool bf16, int rows, int lds, float* theta, float* mom, void* const* reps,
                                double* partials, UnitRecord* rec, int64_t n, double lr, double rho,
                                hipStream_t stream) {
-    return bf16 ? fused_mean_launch<K, true>(rows, theta, mom, reps, partials, rec, n, lr, rho, stream)
-                : fused_mean_launch<K, false>(rows, theta, mom, reps, partials, rec, n, lr, rho, stream);
+    return bf16 ? fused_mean_launch<K, true>(rows, lds, theta, mom, reps, partials, rec, n, lr, rho, stream)
+                : fused_mean_launch<K, false>(rows, lds, theta, mom, reps, partials, rec, n, lr, rho, stream);
   }
   static int pass1_blocks_per_cu(bool bf16) {
     return bf16 ? occupancy(pass1_kernel<K, true>(), pass1_threads<K>())

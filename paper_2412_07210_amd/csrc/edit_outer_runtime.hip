@@ -120,6 +120,7 @@ struct edit_outer {
   int device = 0;
   int num_cu = 0;
   int pass2_lds = 0;       // dynamic LDS per update-pass block (occupancy cap)
+  int fused_lds = 0;       // the same for the one-pass kernel
   int cap1 = 1;            // resident blocks of pass 1 on the whole GPU
   int32_t profile_every = 0;  // record kernel events on units l with l % every == 0
   char* arena = nullptr;   // one device allocation for every unit's scratch
@@ -316,6 +317,7 @@ edit_status_t edit_outer_init(const edit_outer_config_t* cfg, edit_outer_t* out)
       return fail_hip(e, "hipDeviceGetAttribute(LDS per CU)");
     }
     h->pass2_lds = update_pass_lds(K, lds_per_cu);
+    h->fused_lds = one_pass_lds(K, cfg->replica_dtype == EDIT_BF16, lds_per_cu);
   }
   h->noalloc = noalloc;
   const bool bf16 = cfg->replica_dtype == EDIT_BF16;
@@ -542,7 +544,7 @@ struct Enqueue {
   edit_status_t fused(int32_t layer, float* theta, float* momentum, void* const* replicas) {
     Unit& u = h->units[layer];
     void* const* mreps = u.n == 0 ? kNoReplicas : replicas;
-    hipError_t e = launch_fused_mean(K, bf16, u.rows, theta, momentum, mreps, u.partials, u.rec, u.n,
+    hipError_t e = launch_fused_mean(K, bf16, u.rows, h->fused_lds, theta, momentum, mreps, u.partials, u.rec, u.n,
                                      h->cfg.outer_lr, h->cfg.momentum, s);
     return e == hipSuccess ? EDIT_OK : fail_hip(e, "one-pass launch");
   }
