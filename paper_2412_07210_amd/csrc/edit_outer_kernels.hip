@@ -393,20 +393,15 @@ __device__ __forceinline__ void gram_vector(double (&acc)[K * (K + 1) / 2], cons
   }
 }
 
-// theta and every replica at vector v; zeros past the end (they add nothing).
+// theta and every replica at vector v (< nvec).  Unguarded: the caller
+// clamps v, so that no load sits under a lane mask; a masked load makes the
+// compiler wait for the next trip's loads before computing this one.
 template <int K, bool BF16, bool NT>
 __device__ __forceinline__ void load_pass1(const float* theta, const ConstPtrs<K>& reps, int64_t v,
-                                           int64_t nvec, float (&th)[Vec<BF16>::VE], u32x4 (&raw)[K]) {
-  if (v < nvec) {
-    load_f32<Vec<BF16>::VE, NT>(theta, v, th);
+                                           float (&th)[Vec<BF16>::VE], u32x4 (&raw)[K]) {
+  load_f32<Vec<BF16>::VE, NT>(theta, v, th);
 #pragma unroll
-    for (int j = 0; j < K; ++j) raw[j] = ld16<NT>(reinterpret_cast<const u32x4*>(reps.p[j]) + v);
-  } else {
-#pragma unroll
-    for (int e = 0; e < Vec<BF16>::VE; ++e) th[e] = 0.f;
-#pragma unroll
-    for (int j = 0; j < K; ++j) raw[j] = u32x4{0u, 0u, 0u, 0u};
-  }
+  for (int j = 0; j < K; ++j) raw[j] = ld16<NT>(reinterpret_cast<const u32x4*>(reps.p[j]) + v);
 }
 
 template <int K, bool BF16, bool NT>
@@ -514,11 +509,10 @@ __global__ __launch_bounds__(pass1_threads<K>()) void pass1_gram_pair_kernel(Pas
 // loads two trips ahead, measured no faster and need 512-thread blocks).
 constexpr int kMfmaSlots = 1;
 // Load buffers per lane in the matrix-core pass's loop: two (the next trip's
-// loads in flight while one is computed).  Three, four or six buffers at
-// K = 16 (111-165 VGPRs, no spills, up to 3x the bytes in flight) measured
-// the same round time (A/B on one box), so the pass is not waiting on
-// memory latency: its matrix-core and vector instructions share one issue
-// port and take its time.
+// loads in flight while one is computed).  With every load unmasked, three
+// buffers and 1024-thread blocks measured within 1% of this at K = 16 (A/B
+// on one box): the pass is not waiting on memory latency.  Its matrix-core
+// and vector instructions share one issue port and take its time.
 template <int K>
 constexpr int kMfmaDepth() {
   return 2;
@@ -529,6 +523,12 @@ struct Tiles4 {
   static constexpr int G = (K + 3) / 4;      // worker groups of four
   static constexpr int T = G * (G + 1) / 2;  // tiles (I, J), I <= J
 };
+
+// Theta in the matrix-core pass: every lane loads its quad's whole theta
+// vector (true; the four lanes of a quad read the same bytes, which the L1
+// serves), or a quarter of it that DPP moves then broadcast within the quad
+// (false: eight more vector instructions per vector slot).
+constexpr bool kMfmaThetaFull = true;
 
 // Lane src's value within each quad of four lanes (DPP quad permutation).
 __device__ __forceinline__ float quad_bcast(float x, int src) {
@@ -551,37 +551,52 @@ __device__ __forceinline__ float quad_bcast(float x, int src) {
   return __int_as_float(r);
 }
 
-// One vector slot of a quad: lane c's VE/4 theta values (elements
-// c*VE/4 ... of the vector) and its groups' replica vectors.
+// One vector slot of a quad: the theta values lane c holds (the whole
+// vector, or its elements c*VE/4 ...) and its groups' replica vectors.
 template <int G, bool BF16>
 struct Quad4 {
+  static constexpr int TH = kMfmaThetaFull ? Vec<BF16>::VE : Vec<BF16>::VE / 4;
   u32x4 raw[G];
-  float th[Vec<BF16>::VE / 4];
+  float th[TH];
 };
 
+// Vector v (< nvec) of theta and of lane c's replicas.  Lanes of workers
+// >= K (act false, only in the last group when K is not a multiple of 4)
+// feed zeros.  No bounds guard: the caller clamps v, so that no load sits
+// under a lane mask and the loads of later trips stay in flight.
 template <int G, bool BF16, bool NT>
 __device__ __forceinline__ void load_quad4(const float* theta, const void* const (&rep)[G],
-                                           const bool (&act)[G], int c, int64_t v, int64_t nvec,
-                                           Quad4<G, BF16>& q) {
+                                           const bool (&act)[G], int c, int64_t v, Quad4<G, BF16>& q) {
   constexpr int VE = Vec<BF16>::VE;
+  constexpr int TH = Quad4<G, BF16>::TH;
+  const float* tp = theta + v * VE + (kMfmaThetaFull ? 0 : c * TH);
+  if constexpr (TH % 4 == 0) {
+#pragma unroll
+    for (int h = 0; h < TH / 4; ++h) {
+      const f32x4 t = ld16<NT>(reinterpret_cast<const f32x4*>(tp) + h);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) q.th[4 * h + i] = t[i];
+    }
+  } else if constexpr (TH == 2) {
+    const float2_t t2 = NT ? __builtin_nontemporal_load(reinterpret_cast<const float2_t*>(tp))
+                           : *reinterpret_cast<const float2_t*>(tp);
+    q.th[0] = t2[0];
+    q.th[1] = t2[1];
+  } else {
+    q.th[0] = NT ? __builtin_nontemporal_load(tp) : *tp;
+  }
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+    q.raw[g] = act[g] ? ld16<NT>(reinterpret_cast<const u32x4*>(rep[g]) + v) : u32x4{0u, 0u, 0u, 0u};
+}
+
+// A quad whose vector lies past the unit's end contributes nothing.
+template <int G, bool BF16>
+__device__ __forceinline__ void zero_quad4(Quad4<G, BF16>& q) {
 #pragma unroll
   for (int g = 0; g < G; ++g) q.raw[g] = u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int t = 0; t < VE / 4; ++t) q.th[t] = 0.f;
-  if (v < nvec) {
-    const float* tp = theta + v * VE + c * (VE / 4);
-    if constexpr (BF16) {
-      const float2_t t2 = NT ? __builtin_nontemporal_load(reinterpret_cast<const float2_t*>(tp))
-                             : *reinterpret_cast<const float2_t*>(tp);
-      q.th[0] = t2[0];
-      q.th[1] = t2[1];
-    } else {
-      q.th[0] = NT ? __builtin_nontemporal_load(tp) : *tp;
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-      if (act[g]) q.raw[g] = ld16<NT>(reinterpret_cast<const u32x4*>(rep[g]) + v);
-  }
+  for (int t = 0; t < Quad4<G, BF16>::TH; ++t) q.th[t] = 0.f;
 }
 
 // The Gram tiles of one vector slot: theta element e comes from lane
@@ -607,10 +622,14 @@ template <int K, bool BF16>
 __device__ __forceinline__ void gram_quad4_bcast(double (&acc)[Tiles4<K>::T], const Quad4<Tiles4<K>::G, BF16>& q,
                                                  const bool (&act)[Tiles4<K>::G]) {
   constexpr int VE = Vec<BF16>::VE;
-  float th[VE];
+  if constexpr (kMfmaThetaFull) {
+    gram_quad4<K, BF16>(acc, q.raw, q.th, act);
+  } else {
+    float th[VE];
 #pragma unroll
-  for (int e = 0; e < VE; ++e) th[e] = quad_bcast(q.th[e % (VE / 4)], e / (VE / 4));
-  gram_quad4<K, BF16>(acc, q.raw, th, act);
+    for (int e = 0; e < VE; ++e) th[e] = quad_bcast(q.th[e % (VE / 4)], e / (VE / 4));
+    gram_quad4<K, BF16>(acc, q.raw, th, act);
+  }
 }
 
 template <int K, bool BF16, bool NT>
