@@ -86,13 +86,16 @@ int fused_vectors_per_thread(int K, bool bf16) {
 }
 
 // The one-pass kernel streams the same 2K + 4 buffers as the update pass.
-// With bf16 replicas (two 16-byte vectors per thread, 3 waves per SIMD by
-// its registers) four resident blocks per CU measured best at the 1B shape:
-// 10.64-10.73 ms per round against 11.02-11.07 ms uncapped, 10.86-10.93 at
-// three blocks and 15.4 at two (A/B runs on one box).  Other cases keep the
-// occupancy their registers give.
+// With bf16 replicas (two 16-byte vectors per thread) and one-wave blocks,
+// six resident blocks per CU measured best at the 1B shape (rocprofv3, A/B
+// runs on one box): 435 us per unit against 438-442 at five or seven blocks
+// and 441 for 128-thread blocks at four per CU (the earlier shape, itself
+// 10.64-10.73 ms per round against 11.02-11.07 uncapped).  One vector per
+// thread took 474-484 us: each block's closing reduction and partial row
+// then cover half as much data.  Other cases keep the occupancy their
+// registers give.
 int one_pass_lds(int K, bool bf16, int lds_per_cu) {
-  const int blocks = bf16 && K <= 16 ? 4 : 0;
+  const int blocks = bf16 && K <= 16 ? 6 : 0;
   return blocks > 0 && lds_per_cu > 0 ? (lds_per_cu / blocks) & ~255 : 0;
 }
 

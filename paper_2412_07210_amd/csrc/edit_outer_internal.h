@@ -11,7 +11,7 @@ namespace edit {
 
 constexpr int kThreads = 256;        // threads per block of the Gram pass
 constexpr int kPass2Threads = 64;    // threads per block of the update pass (one wave)
-constexpr int kFusedThreads = 128;   // threads per block of the one-pass mean step
+constexpr int kFusedThreads = 64;    // threads per block of the one-pass mean step (one wave)
 constexpr int kMaxK = EDIT_MAX_K;
 constexpr int kMaxPairs = kMaxK * (kMaxK + 1) / 2;
 
