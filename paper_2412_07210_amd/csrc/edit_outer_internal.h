@@ -152,7 +152,7 @@ int update_pass_blocks_per_cu(int K);
 int update_pass_lds(int K, int lds_per_cu);
 // One-pass mean step (no penalty components): `rows` blocks of
 // fused_vectors_per_thread(K, bf16) * kFusedThreads vectors each, leaving
-// (K+1) x rows norm partials and the unit marked; then one block per entry
+// rows x (K+1) norm partials (each block's K+1 sums contiguous) and the unit marked; then one block per entry
 // of `table` turns marked units' partials into their records.
 int fused_vectors_per_thread(int K, bool bf16);
 // `lds`: dynamic LDS per block capping its resident blocks per CU

@@ -524,67 +524,26 @@ struct Tiles4 {
   static constexpr int T = G * (G + 1) / 2;  // tiles (I, J), I <= J
 };
 
-// Theta in the matrix-core pass: every lane loads its quad's whole theta
-// vector (true; the four lanes of a quad read the same bytes, which the L1
-// serves), or a quarter of it that DPP moves then broadcast within the quad
-// (false: eight more vector instructions per vector slot).
-constexpr bool kMfmaThetaFull = true;
-
-// Lane src's value within each quad of four lanes (DPP quad permutation).
-__device__ __forceinline__ float quad_bcast(float x, int src) {
-  const int xi = __float_as_int(x);
-  int r;
-  switch (src) {
-    case 0:
-      r = __builtin_amdgcn_mov_dpp(xi, 0x00, 0xf, 0xf, false);
-      break;
-    case 1:
-      r = __builtin_amdgcn_mov_dpp(xi, 0x55, 0xf, 0xf, false);
-      break;
-    case 2:
-      r = __builtin_amdgcn_mov_dpp(xi, 0xaa, 0xf, 0xf, false);
-      break;
-    default:
-      r = __builtin_amdgcn_mov_dpp(xi, 0xff, 0xf, 0xf, false);
-      break;
-  }
-  return __int_as_float(r);
-}
-
-// One vector slot of a quad: the theta values lane c holds (the whole
-// vector, or its elements c*VE/4 ...) and its groups' replica vectors.
+// One vector slot of a quad: the whole theta vector (every lane of the quad
+// loads it; the L1 serves the repeats, which measured faster than loading a
+// quarter per lane and broadcasting it by DPP moves, eight more vector
+// instructions per slot) and lane c's groups' replica vectors.
 template <int G, bool BF16>
 struct Quad4 {
-  static constexpr int TH = kMfmaThetaFull ? Vec<BF16>::VE : Vec<BF16>::VE / 4;
+  static constexpr int TH = Vec<BF16>::VE;
   u32x4 raw[G];
   float th[TH];
 };
 
-// Vector v (< nvec) of theta and of lane c's replicas.  Lanes of workers
-// >= K (act false, only in the last group when K is not a multiple of 4)
-// feed zeros.  No bounds guard: the caller clamps v, so that no load sits
-// under a lane mask and the loads of later trips stay in flight.
+// Vector v (< nvec) of theta and of this lane's replicas (rep[g] is worker
+// 4g + lane % 4).  Lanes of workers >= K (act false, only in the last group
+// when K is not a multiple of 4) feed zeros.  No bounds guard: the caller
+// clamps v, so that no load sits under a lane mask and the loads of later
+// trips stay in flight.
 template <int G, bool BF16, bool NT>
 __device__ __forceinline__ void load_quad4(const float* theta, const void* const (&rep)[G],
-                                           const bool (&act)[G], int c, int64_t v, Quad4<G, BF16>& q) {
-  constexpr int VE = Vec<BF16>::VE;
-  constexpr int TH = Quad4<G, BF16>::TH;
-  const float* tp = theta + v * VE + (kMfmaThetaFull ? 0 : c * TH);
-  if constexpr (TH % 4 == 0) {
-#pragma unroll
-    for (int h = 0; h < TH / 4; ++h) {
-      const f32x4 t = ld16<NT>(reinterpret_cast<const f32x4*>(tp) + h);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) q.th[4 * h + i] = t[i];
-    }
-  } else if constexpr (TH == 2) {
-    const float2_t t2 = NT ? __builtin_nontemporal_load(reinterpret_cast<const float2_t*>(tp))
-                           : *reinterpret_cast<const float2_t*>(tp);
-    q.th[0] = t2[0];
-    q.th[1] = t2[1];
-  } else {
-    q.th[0] = NT ? __builtin_nontemporal_load(tp) : *tp;
-  }
+                                           const bool (&act)[G], int64_t v, Quad4<G, BF16>& q) {
+  load_f32<Vec<BF16>::VE, NT>(theta, v, q.th);
 #pragma unroll
   for (int g = 0; g < G; ++g)
     q.raw[g] = act[g] ? ld16<NT>(reinterpret_cast<const u32x4*>(rep[g]) + v) : u32x4{0u, 0u, 0u, 0u};
@@ -599,8 +558,8 @@ __device__ __forceinline__ void zero_quad4(Quad4<G, BF16>& q) {
   for (int t = 0; t < Quad4<G, BF16>::TH; ++t) q.th[t] = 0.f;
 }
 
-// The Gram tiles of one vector slot: theta element e comes from lane
-// e / (VE/4) of the quad.
+// The Gram tiles of one vector slot: for each of its VE elements, the
+// lane's group deltas (exact, fp64) go into every tile (I, J), I <= J.
 template <int K, bool BF16>
 __device__ __forceinline__ void gram_quad4(double (&acc)[Tiles4<K>::T], const u32x4 (&raw)[Tiles4<K>::G],
                                            const float (&th)[Vec<BF16>::VE], const bool (&act)[Tiles4<K>::G]) {
@@ -615,20 +574,6 @@ __device__ __forceinline__ void gram_quad4(double (&acc)[Tiles4<K>::T], const u3
     for (int I = 0; I < G; ++I)
 #pragma unroll
       for (int J = I; J < G; ++J, ++t) acc[t] = __builtin_amdgcn_mfma_f64_4x4x4f64(d[I], d[J], acc[t], 0, 0, 0);
-  }
-}
-
-template <int K, bool BF16>
-__device__ __forceinline__ void gram_quad4_bcast(double (&acc)[Tiles4<K>::T], const Quad4<Tiles4<K>::G, BF16>& q,
-                                                 const bool (&act)[Tiles4<K>::G]) {
-  constexpr int VE = Vec<BF16>::VE;
-  if constexpr (kMfmaThetaFull) {
-    gram_quad4<K, BF16>(acc, q.raw, q.th, act);
-  } else {
-    float th[VE];
-#pragma unroll
-    for (int e = 0; e < VE; ++e) th[e] = quad_bcast(q.th[e % (VE / 4)], e / (VE / 4));
-    gram_quad4<K, BF16>(acc, q.raw, th, act);
   }
 }
 
@@ -915,7 +860,6 @@ __global__ __launch_bounds__(kFusedThreads) void fused_mean_kernel(float* __rest
                                                                    double lr, double rho) {
   constexpr int VE = Vec<BF16>::VE;
   constexpr double inv_k = 1.0 / K;
-  const int rows = gridDim.x;
   const int b = blockIdx.x;
   double sq[K + 1];  // sum of Delta_j^2 per worker, then of Delta_bar^2
 #pragma unroll
@@ -991,11 +935,11 @@ __global__ __launch_bounds__(kFusedThreads) void fused_mean_kernel(float* __rest
     if (lane == 0) red[wave][p] = t;
   }
   __syncthreads();
-  if (threadIdx.x <= K) {
+  if (threadIdx.x <= K) {  // the block's K + 1 sums, contiguous
     double t = red[0][threadIdx.x];
 #pragma unroll
     for (int w = 1; w < kWaves; ++w) t += red[w][threadIdx.x];
-    partials[static_cast<int64_t>(threadIdx.x) * rows + b] = t;
+    partials[static_cast<int64_t>(b) * (K + 1) + threadIdx.x] = t;
   }
   if (b == 0 && threadIdx.x == 0) rec->finish_pending = 1;
 }
@@ -1024,7 +968,7 @@ __global__ __launch_bounds__(kDecideThreads) void fused_finish_kernel(const Fini
 #pragma unroll 4
   for (int r = threadIdx.x; r < rows; r += kDecideThreads)
 #pragma unroll
-    for (int q = 0; q < NV; ++q) s[q] += partials[static_cast<int64_t>(q) * rows + r];
+    for (int q = 0; q < NV; ++q) s[q] += partials[static_cast<int64_t>(r) * NV + q];
 #pragma unroll
   for (int q = 0; q < NV; ++q) {
     const double t = wave_sum(s[q]);
@@ -1084,8 +1028,6 @@ __global__ __launch_bounds__(kThreads) void copy_kernel(u32x4* __restrict__ dst,
 constexpr bool kNT1 = true;
 constexpr bool kNTMfma = false;  // see pass1_gram_mfma_kernel
 constexpr bool kNT2 = true;
-constexpr int kUnrollCopy = 1;
-constexpr bool kNTCopy = false;
 
 namespace {
 
@@ -1337,6 +1279,9 @@ const KernelSet* EDIT_KERNEL_SET_FN(EDIT_K_FIRST)(int K) {
 }
 
 #if EDIT_K_FIRST == 1  // the copy probe is compiled into one object only
+constexpr int kUnrollCopy = 1;
+constexpr bool kNTCopy = false;
+
 hipError_t launch_copy(void* dst, const void* src, int64_t nbytes, int blocks, hipStream_t stream) {
   hipLaunchKernelGGL((copy_kernel<kUnrollCopy, kNTCopy>), dim3(blocks), dim3(kThreads), 0, stream,
                      reinterpret_cast<u32x4*>(dst), reinterpret_cast<const u32x4*>(src), nbytes / 16);
