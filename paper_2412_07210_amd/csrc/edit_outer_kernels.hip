@@ -958,27 +958,34 @@ __global__ __launch_bounds__(kDecideThreads) void fused_finish_kernel(const Fini
   const double* partials = ent.partials;
   const int rows = ent.rows;
   constexpr int NV = K + 1;
-  constexpr int kWaves = kDecideThreads / 64;
-  __shared__ double red[kWaves][NV];
+  // The partials are rows x NV contiguous doubles.  Thread t reads the flat
+  // array at t, t + S, t + 2S, ... with S a multiple of NV, so it always
+  // reads column t % NV and a wave's loads are contiguous; U loads per
+  // thread are in flight at a time.  The S threads' sums are then added per
+  // column in thread order (a fixed order).
+  constexpr int S = NV * (kDecideThreads / NV);
+  constexpr int U = 16;
+  __shared__ double part[kDecideThreads];
   __shared__ double tot[NV];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  double s[NV];
+  const int64_t total = static_cast<int64_t>(rows) * NV;
+  double s = 0.0;
+  if (threadIdx.x < S) {
+    for (int64_t i = threadIdx.x; i < total; i += int64_t(S) * U) {
+      double v[U];
 #pragma unroll
-  for (int q = 0; q < NV; ++q) s[q] = 0.0;
-#pragma unroll 4
-  for (int r = threadIdx.x; r < rows; r += kDecideThreads)
+      for (int u = 0; u < U; ++u) {
+        const int64_t idx = i + int64_t(u) * S;
+        v[u] = idx < total ? partials[idx] : 0.0;
+      }
 #pragma unroll
-    for (int q = 0; q < NV; ++q) s[q] += partials[static_cast<int64_t>(r) * NV + q];
-#pragma unroll
-  for (int q = 0; q < NV; ++q) {
-    const double t = wave_sum(s[q]);
-    if (lane == 0) red[wave][q] = t;
+      for (int u = 0; u < U; ++u) s += v[u];
+    }
   }
+  part[threadIdx.x] = s;
   __syncthreads();
   if (threadIdx.x < NV) {
-    double t = red[0][threadIdx.x];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) t += red[w][threadIdx.x];
+    double t = 0.0;
+    for (int k = threadIdx.x; k < S; k += NV) t += part[k];
     tot[threadIdx.x] = t;
   }
   __syncthreads();
