@@ -19,7 +19,7 @@ from paper_2412_07210_amd import AE, ONE_PASS, min_warmup, synth
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
-CASES = 48
+CASES = 200
 
 
 def _draw(i):
