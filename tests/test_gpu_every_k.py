@@ -9,13 +9,14 @@ group of vectors cut short by the unit's end, and a ragged tail) and a
 2,051-element unit of at most 256 vectors, stepped whole in a small launch.
 Replicas alternate between bf16 and fp32 with K; the last round scales the
 last worker x40, which the z-test must flag on the larger unit while every
-other worker passes.
+other worker passes.  The one-pass mean step runs for every K on the same
+units, with the replica type the other way round.
 """
 import numpy as np
 import pytest
 
 from parity import NearTie, ParityRun, steady_ema
-from paper_2412_07210_amd import synth
+from paper_2412_07210_amd import ONE_PASS, synth
 from paper_2412_07210_amd.outer import MAX_K
 
 pytestmark = pytest.mark.gpu
@@ -45,5 +46,19 @@ def test_every_worker_count(K):
                 assert flagged == bad, f"K={K} round {t}: flagged {flagged}, expected {bad}"
     except NearTie as e:
         pytest.skip(str(e))
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("K", range(1, MAX_K + 1))
+def test_every_worker_count_one_pass(K):
+    """The one-pass mean step (EDIT_ONE_PASS: no penalty component, the
+    DiLoCo outer step) for every K on the same two units, two rounds."""
+    dtype = "f32" if K % 2 else "bf16"
+    wl = synth.small("llama1b-k8-bf16", SIZES, num_workers=K, replica_dtype=dtype, name=f"everyk1p{K}{dtype}")
+    run = ParityRun(wl, range(len(SIZES)), DEV, flags=ONE_PASS)
+    try:
+        for t in range(2):
+            run.round(t, via_round=True, verbose=False)
     finally:
         run.close()
