@@ -29,7 +29,7 @@ def _inputs(wl, u, t):
 
 
 @pytest.mark.parametrize("one_pass", [False, True])
-@pytest.mark.parametrize("K,dtype", [(8, "bf16"), (4, "f32"), (16, "bf16")])
+@pytest.mark.parametrize("K,dtype", [(8, "bf16"), (4, "f32"), (16, "bf16"), (32, "bf16")])
 def test_host_round_matches_resident_round(K, dtype, one_pass):
     """Six units of mixed sizes (more than the three staging slots) in a
     non-index order, three rounds: theta, b, replicas and records equal the

@@ -108,7 +108,8 @@ def _sharded_rounds(wl, shards, rounds, ema=None, verbose=True, scale=None):
         lib.close()
 
 
-@pytest.mark.parametrize("K,dtype", [(4, "f32"), (8, "bf16"), (11, "bf16"), (16, "bf16")])
+@pytest.mark.parametrize("K,dtype", [(4, "f32"), (8, "bf16"), (11, "bf16"), (16, "bf16"), (24, "bf16"),
+                                     (32, "f32")])
 @pytest.mark.parametrize("shards", [(40000, 33333, 26670), (100003, 0), (8, 99995)])
 def test_sharded_module_matches_unsplit_oracle(K, dtype, shards):
     """Three-way ragged split, an empty shard, and an 8-element shard.  Two
@@ -142,7 +143,8 @@ def test_sharded_module_rollback_and_clip():
 
 
 @pytest.mark.parametrize("K,dtype,n", [(8, "bf16", 3_000_017), (4, "f32", 1_000_005),
-                                       (16, "bf16", 2_000_003), (11, "f32", 65_537)])
+                                       (16, "bf16", 2_000_003), (11, "f32", 65_537),
+                                       (21, "f32", 300_001), (32, "bf16", 1_000_003)])
 def test_gram_then_apply_is_step_layer_bitwise(K, dtype, n):
     """For an unsplit unit the two-call path is the one-call path, bit for bit:
     a warm-up round, then two rounds with three x30 workers."""
