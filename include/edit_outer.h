@@ -284,7 +284,10 @@ const char *edit_outer_last_error(void);
  * partials (nothing in it needs clearing: a call writes every partial it
  * reads).  Calls on one GPU must therefore not overlap: order them on one
  * stream or with events, also across handles and host threads; overlapping
- * calls race. */
+ * calls race.  The call enqueues three kernels and one event record and
+ * makes no synchronising call, so it can be captured into a HIP graph and
+ * replayed; after a replay, once the caller has synchronised,
+ * edit_outer_state_get reports that replay's step. */
 edit_status_t edit_outer_step_layer_noalloc(edit_outer_t h, int32_t layer, float *theta,
                                             float *momentum, void *const *replicas, void *stream);
 
