@@ -5,7 +5,6 @@ cases run units of each workload at their real shapes, through a handle
 configured with every unit of the workload and stepped by
 edit_outer_step_round, i.e. the launch configuration the benchmark times.
 """
-import math
 
 import numpy as np
 import pytest
